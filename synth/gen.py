@@ -1,0 +1,127 @@
+"""Seeded synthetic inputs for the W4A16 linear layer.
+
+Shared by the tests, ``bench.py`` and ``__graft_entry__.smoke()``.  This module
+only draws random numbers and converts them to storage formats; it holds none
+of the layer's arithmetic (no unpacking, dequantization or matmul).
+
+The paper's own data (its model weights, datasets and benchmarks) is not
+available, so every workload is synthetic with the shapes of a 4B-parameter
+decoder (hidden 2560, intermediate 9728, 36 layers) and these distributions:
+
+* codes: uniform over [0, 15].  Eight uniform 4-bit codes packed per uint32
+  are exactly a uniform random uint32, so words are drawn directly.
+* scales: uniform U(a, b) drawn in binary32, then rounded to bf16.
+* zero-points: uniform over {7, 8, 9}, stored as bf16.
+* activations: N(0, sigma^2) drawn in binary32 (sigma is the standard
+  deviation), optionally with each entry independently multiplied by 20 with
+  probability p (activation outliers), then rounded to bf16.
+
+Draw order inside one generator: packed words, scales, zeros, activations,
+outlier mask.  bf16 rounding of drawn values uses torch's conversion.
+"""
+
+import numpy as np
+
+GROUP = 128
+
+# (name, K, N) of the linears in one decoder layer of the 4B-shaped model.
+LAYER_SHAPES = (
+    ("q", 2560, 4096),
+    ("k", 2560, 1024),
+    ("v", 2560, 1024),
+    ("o", 4096, 2560),
+    ("gate_up", 2560, 19456),
+    ("down", 9728, 2560),
+)
+N_LAYERS = 36
+
+# Workloads.  "single" workloads name one linear; "model" covers all 216.
+CONFIGS = {
+    0: dict(name="single-linear M=1 K=2560 N=2560", Ms=(1,), K=2560, N=2560,
+            s_range=(0.002, 0.02), sigma=1.0, outlier_p=0.0, seed=0),
+    1: dict(name="draft-block verify M=16 K=2560 N=19456 (fused gate+up)", Ms=(16,),
+            K=2560, N=19456, s_range=(0.002, 0.02), sigma=1.0, outlier_p=0.0, seed=1),
+    2: dict(name="ffn-down M=1/4/8/16 K=9728 N=2560 with outliers", Ms=(1, 4, 8, 16),
+            K=9728, N=2560, s_range=(0.001, 0.01), sigma=0.5, outlier_p=0.01, seed=2),
+    3: dict(name="36-layer 4B decoder weight pass M=16", Ms=(16,), model=True,
+            s_range=(0.002, 0.02), sigma=1.0, outlier_p=0.0, seed=3),
+    4: dict(name="chunked prefill M=128/512/2048 over the 36-layer weights",
+            Ms=(128, 512, 2048), model=True, s_range=(0.002, 0.02), sigma=1.0,
+            outlier_p=0.0, seed=4),
+}
+
+
+def f32_to_bf16_bits(a):
+    """binary32 array -> bf16 bit patterns (uint16), via torch's RNE conversion."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    return t.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16).copy()
+
+
+def draw_weights(rng, K, N, s_range, z_values=(7, 8, 9), group=GROUP):
+    """Packed codes [N][K/8] uint32, scales and zeros [N][K/group] bf16 bits."""
+    packed = rng.integers(0, 2 ** 32, size=(N, K // 8), dtype=np.uint32)
+    lo, hi = s_range
+    scales = f32_to_bf16_bits(rng.uniform(lo, hi, size=(N, K // group)).astype(np.float32))
+    zeros = f32_to_bf16_bits(
+        np.asarray(z_values, dtype=np.float32)[rng.integers(0, len(z_values), size=(N, K // group))])
+    return packed, scales, zeros
+
+
+def draw_activations(rng, M, K, sigma=1.0, outlier_p=0.0, outlier_mul=20.0):
+    """Activations x[M][K] as bf16 bits (outliers scaled before rounding)."""
+    x = rng.standard_normal((M, K), dtype=np.float32) * np.float32(sigma)
+    if outlier_p > 0.0:
+        mask = rng.random((M, K)) < outlier_p
+        x = np.where(mask, x * np.float32(outlier_mul), x).astype(np.float32)
+    return f32_to_bf16_bits(x)
+
+
+def linear_case(cfg_id, M=None):
+    """One linear of a single-linear workload (configs 0, 1, 2).
+
+    Returns dict(M, K, N, packed, scales, zeros, x).  For config 2 the
+    activations are drawn once for the largest M and smaller M take the
+    leading rows.
+    """
+    c = CONFIGS[cfg_id]
+    if c.get("model"):
+        raise ValueError("use model_linear() for whole-model workloads")
+    rng = np.random.default_rng(c["seed"])
+    packed, scales, zeros = draw_weights(rng, c["K"], c["N"], c["s_range"])
+    Mmax = max(c["Ms"])
+    x = draw_activations(rng, Mmax, c["K"], c["sigma"], c["outlier_p"])
+    M = Mmax if M is None else M
+    if M > Mmax:
+        raise ValueError("M larger than the workload's")
+    return dict(M=M, K=c["K"], N=c["N"], packed=packed, scales=scales,
+                zeros=zeros, x=np.ascontiguousarray(x[:M]))
+
+
+def model_linear_seed(layer, proj):
+    """Seed of linear ``proj`` (index into LAYER_SHAPES) of decoder ``layer``."""
+    return 3_000_000 + 10 * layer + proj
+
+
+def model_linear(layer, proj):
+    """Weights of one linear of the 36-layer model (configs 3 and 4)."""
+    name, K, N = LAYER_SHAPES[proj]
+    rng = np.random.default_rng(model_linear_seed(layer, proj))
+    packed, scales, zeros = draw_weights(rng, K, N, CONFIGS[3]["s_range"])
+    return dict(name=name, K=K, N=N, packed=packed, scales=scales, zeros=zeros)
+
+
+def model_activations(cfg_id, M, K):
+    """Activations for the whole-model workloads: one x per (M, K)."""
+    c = CONFIGS[cfg_id]
+    rng = np.random.default_rng([c["seed"], M, K])
+    return draw_activations(rng, M, K, c["sigma"], c["outlier_p"])
+
+
+def random_case(seed, M, K, N, s_range=(0.002, 0.02), z_values=(7, 8, 9),
+                sigma=1.0, outlier_p=0.0):
+    """A generic seeded case for tests at arbitrary (small) shapes."""
+    rng = np.random.default_rng(seed)
+    packed, scales, zeros = draw_weights(rng, K, N, s_range, z_values)
+    x = draw_activations(rng, M, K, sigma, outlier_p)
+    return dict(M=M, K=K, N=N, packed=packed, scales=scales, zeros=zeros, x=x)
