@@ -1,0 +1,152 @@
+/*
+ * qlin.h -- C ABI of the MI355X (gfx950) weight-only INT4 linear layer (W4A16).
+ *
+ * The operation (Kim, Lee, Kim, "Quantize the Target, Quantize the Drafter",
+ * arXiv 2607.04244):
+ *   Sec. 2.1  the served model keeps INT4 codes W_q with frozen per-group
+ *             scales s; the dequantized weight is W = s (.) W_q and the model
+ *             runs in the W4A16 format (4-bit weights, 16-bit activations).
+ *   Sec. 3.2  the INT4 grid is dequantized into floating point: the matmul
+ *             sees bf16 weights.
+ *   Sec. 3.3  groups of 128 consecutive input features share one scale.
+ *   Sec. 2.2, 3.2, 3.3  the target verifies, and the drafter proposes, one
+ *             16-token block per speculative step, so the layer runs at small
+ *             row counts M (16 per block, 1 for plain decode).
+ *
+ * Computed here, for every m < M, n < N:
+ *   w[n][k]  = RNE_bf16( (q[n][k] - z[n][k/128]) * s[n][k/128] )
+ *   y[m][n]  = RNE_bf16( sum_k x[m][k] * w[n][k] )      (fp32 accumulation)
+ * with unsigned codes q in [0, 15] and zero-points z; the paper's symmetric
+ * format is z = 8 (see qlin_create_symmetric).
+ *
+ * Conventions: all tensors are row-major and contiguous; bf16 values travel
+ * as uint16_t bit patterns; every call returns a QLIN_* status except
+ * qlin_create* (NULL on failure) and qlin_destroy.  Argument checks run
+ * before any HIP call.  The library never aborts and never prints.  After a
+ * failure, qlin_last_error() returns a message for the calling thread.
+ */
+#ifndef QLIN_H
+#define QLIN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct qlin_s *qlin_t;   /* opaque; immutable after creation */
+
+enum {
+    QLIN_OK = 0,
+    QLIN_ERR_INVALID = -1,      /* bad argument (size, NULL, aliasing, zero-point value) */
+    QLIN_ERR_UNSUPPORTED = -2,  /* valid but outside this build (group != 128, N % 16, scale range, M) */
+    QLIN_ERR_ALIGN = -3,        /* x or y not 16-byte aligned */
+    QLIN_ERR_OOM = -4,          /* device allocation failed */
+    QLIN_ERR_HIP = -5           /* a HIP runtime call or kernel launch failed */
+};
+
+/* Kernel paths for qlin_forward_path (qlin_forward picks one itself). */
+enum {
+    QLIN_PATH_AUTO = 0,
+    QLIN_PATH_GEMV = 1,    /* vector-ALU dequantize + v_dot2 dot product, M <= 8 */
+    QLIN_PATH_SKINNY = 2,  /* matrix-core dequantize + MFMA 16x16x32, M <= 64 */
+    QLIN_PATH_TILED = 3    /* LDS-tiled MFMA GEMM for prefill-sized M */
+};
+
+/*
+ * qlin_create -- build a handle for one linear layer (K inputs, N outputs).
+ *
+ *   packed_w  HOST  uint32 [N][K/8]; code of (n, k = 8j + i) is
+ *                   (packed_w[n*K/8 + j] >> 4i) & 0xF (lowest nibble = lowest k)
+ *   scales    HOST  bf16 [N][K/group]; positive normal numbers in [2^-100, 2^100]
+ *   zeros     HOST  bf16 [N][K/group]; integer values in [0, 15]
+ *   group     must be 128 (Sec. 3.3)
+ *
+ * Constraints: K > 0, N > 0, K % 128 == 0, N % 16 == 0, K <= 65536,
+ * N <= 1048576.  The call copies and re-lays-out the weights into device
+ * memory owned by the handle on the current device and returns after that
+ * work has finished, so the caller may free its buffers at once.
+ * Errors: NULL with qlin_last_error() set (INVALID / UNSUPPORTED / OOM / HIP).
+ * Not thread-safe with respect to other HIP work on the default stream.
+ */
+qlin_t qlin_create(int64_t K, int64_t N, int64_t group,
+                   const uint32_t *packed_w, const uint16_t *scales,
+                   const uint16_t *zeros);
+
+/*
+ * qlin_create_symmetric -- the paper's symmetric format (Sec. 2.1 "symmetric
+ * per-group scales", Sec. 3.3 "group-wise symmetric INT4"): no zero-point
+ * tensor; the signed code W_q in [-8, 7] is stored as the nibble W_q + 8, so
+ * w = RNE_bf16((q - 8) * s).  Same arguments and rules as qlin_create.
+ */
+qlin_t qlin_create_symmetric(int64_t K, int64_t N, int64_t group,
+                             const uint32_t *packed_w, const uint16_t *scales);
+
+/*
+ * qlin_forward -- y[M][N] = x[M][K] . w^T as defined above (asynchronous).
+ *
+ *   x       DEVICE bf16 [M][K], 16-byte aligned, read-only
+ *   y       DEVICE bf16 [M][N], 16-byte aligned, must not overlap x
+ *   stream  hipStream_t to launch on; NULL = the default stream
+ *
+ * M = 0 is a no-op returning QLIN_OK.  0 < M <= 65536.  x and y must stay
+ * valid until the stream's work completes.  The handle owns a small
+ * workspace, so one handle must not run on two streams at the same time
+ * (different handles are independent).  The device current at call time
+ * must be the handle's device.
+ * Errors: INVALID (NULL, M < 0, overlap, wrong device), UNSUPPORTED (M too
+ * large), ALIGN, HIP.
+ */
+int qlin_forward(qlin_t h, int64_t M, const uint16_t *x, uint16_t *y, void *stream);
+
+/*
+ * qlin_forward_path -- qlin_forward with the kernel path and the number of
+ * K-chunks (split_k; 0 = the planner's choice) forced, for tests and tuning.
+ * Errors as qlin_forward, plus INVALID for an unknown path, split_k < 0 or
+ * split_k > K/128, and UNSUPPORTED when the path cannot run this M
+ * (GEMV: M <= 8; SKINNY: M <= 64).
+ */
+int qlin_forward_path(qlin_t h, int path, int64_t split_k, int64_t M,
+                      const uint16_t *x, uint16_t *y, void *stream);
+
+/*
+ * qlin_plan -- describe, without launching, what qlin_forward_path would run
+ * for (path, split_k, M): writes a NUL-terminated text such as
+ * "path=skinny kernel=qlin_skinny_mt1 grid=256 block=512 split=1 lds=88064"
+ * into buf (at most buflen bytes).  Returns QLIN_OK or an error as
+ * qlin_forward_path.
+ */
+int qlin_plan(qlin_t h, int path, int64_t split_k, int64_t M, char *buf, int64_t buflen);
+
+/* qlin_destroy -- wait for the device to finish the handle's work, free it. NULL-safe. */
+void qlin_destroy(qlin_t h);
+
+/* qlin_last_error -- message of the calling thread's last failure ("" if none). */
+const char *qlin_last_error(void);
+
+/* qlin_last_status -- QLIN_* code of the calling thread's last call (QLIN_OK if it
+ * succeeded); the way to learn why qlin_create* returned NULL. */
+int qlin_last_status(void);
+
+/*
+ * Test hooks.  Both read the handle's device layout with the same device
+ * routines the forward kernels use, so comparing them with the oracle
+ * checks the layout and the dequantization bit by bit.
+ *
+ * qlin_unpack_codes: q_out DEVICE uint8 [N][K], codes in [0, 15].
+ * qlin_dequantize:   w_out DEVICE bf16 [N][K]; routine 0 = the matrix-core
+ *                    routine (SKINNY/TILED paths), 1 = the vector-ALU routine
+ *                    (GEMV path).  Both must give identical bits.
+ * Outputs must be 16-byte aligned.  Asynchronous on stream.
+ */
+int qlin_unpack_codes(qlin_t h, uint8_t *q_out, void *stream);
+int qlin_dequantize(qlin_t h, int routine, uint16_t *w_out, void *stream);
+
+/* qlin_shape -- K and N of a handle (either pointer may be NULL). */
+int qlin_shape(qlin_t h, int64_t *K, int64_t *N);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QLIN_H */

@@ -1,0 +1,412 @@
+// C ABI of the W4A16 linear layer: argument checks, handle ownership, the
+// M-dispatch / work planner and the launches.  Declared in include/qlin.h.
+
+#include "../../include/qlin.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <mutex>
+
+#include "qlin_internal.h"
+
+using namespace qlin;
+
+struct qlin_s {
+    int device = -1;
+    int num_cu = 0;
+    int64_t K = 0, N = 0;
+    int Kb = 0, Nt = 0;
+    bool symmetric = false;
+    uint4 *codes = nullptr;      // Nt * Kb blocks of 1 KiB
+    void *sz = nullptr;          // Nt * Kb * 16 entries (u32 s|z<<16, or u16 s)
+    float *ws = nullptr;         // split-K partials, ws_rows * N floats
+    int ws_rows = 0;             // bound on S * M of any plan
+    uint32_t *counters = nullptr;
+    int counters_n = 0;
+};
+
+namespace {
+
+constexpr int kWsRowsMin = 128;        // S * M always allowed by the partial-sum workspace
+constexpr size_t kXLdsBudget = 128 * 1024;   // LDS for the staged x chunk (rest: accumulators)
+constexpr int64_t kMaxK = 65536, kMaxN = 1 << 20, kMaxM = 65536;
+
+thread_local char g_err[512] = "";
+thread_local int g_status = QLIN_OK;
+
+int fail(int code, const char *fmt, ...) {
+    g_status = code;
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+void clear_err() {
+    g_err[0] = 0;
+    g_status = QLIN_OK;
+}
+
+int hip_fail(hipError_t e, const char *what) {
+    return fail(QLIN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Test hook: QLIN_FAULT=alloc makes every device allocation of this library fail.
+hipError_t dev_alloc(void **p, size_t bytes) {
+    const char *f = getenv("QLIN_FAULT");
+    if (f && strcmp(f, "alloc") == 0) {
+        *p = nullptr;
+        return hipErrorOutOfMemory;
+    }
+    return hipMalloc(p, bytes);
+}
+
+float bf16_value(uint16_t b) {
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+}
+
+int check_shape(int64_t K, int64_t N, int64_t group) {
+    if (K <= 0 || N <= 0 || group <= 0) return fail(QLIN_ERR_INVALID, "K, N and group must be positive");
+    if (group != kGroup) return fail(QLIN_ERR_UNSUPPORTED, "group must be 128 (got %lld)", (long long)group);
+    if (K % group) return fail(QLIN_ERR_INVALID, "K (%lld) must be a multiple of the group size", (long long)K);
+    if (N % kTileN) return fail(QLIN_ERR_UNSUPPORTED, "N (%lld) must be a multiple of 16", (long long)N);
+    if (K > kMaxK || N > kMaxN) return fail(QLIN_ERR_UNSUPPORTED, "K <= 65536 and N <= 1048576 required");
+    return QLIN_OK;
+}
+
+// Scales must be positive normal bf16 numbers in [2^-100, 2^100]: inside that
+// range every (128 + q) * s and (q - z) * s is an exact binary32 number, which
+// is what makes the matrix-core dequantization exact.
+int check_scales(const uint16_t *s, size_t n) {
+    for (size_t i = 0; i < n; ++i) {
+        const int e = (s[i] >> 7) & 0xFF;
+        if ((s[i] & 0x8000) || e < 127 - 100 || e > 127 + 99)
+            return fail(QLIN_ERR_UNSUPPORTED, "scale %zu (0x%04x) outside [2^-100, 2^100] or not positive", i,
+                        (unsigned)s[i]);
+    }
+    return QLIN_OK;
+}
+
+int check_zeros(const uint16_t *z, size_t n) {
+    for (size_t i = 0; i < n; ++i) {
+        const float v = bf16_value(z[i]);
+        if (!(v >= 0.0f && v <= 15.0f) || v != std::floor(v))
+            return fail(QLIN_ERR_INVALID, "zero-point %zu (0x%04x) is not an integer in [0, 15]", i, (unsigned)z[i]);
+    }
+    return QLIN_OK;
+}
+
+void free_handle(qlin_s *h) {
+    if (!h) return;
+    if (h->codes) (void)hipFree(h->codes);
+    if (h->sz) (void)hipFree(h->sz);
+    if (h->ws) (void)hipFree(h->ws);
+    if (h->counters) (void)hipFree(h->counters);
+    delete h;
+}
+
+qlin_t create_impl(int64_t K, int64_t N, int64_t group, const uint32_t *packed, const uint16_t *scales,
+                   const uint16_t *zeros, bool symmetric) {
+    clear_err();
+    if (check_shape(K, N, group) != QLIN_OK) return nullptr;
+    if (!packed || !scales || (!symmetric && !zeros)) {
+        fail(QLIN_ERR_INVALID, "NULL weight pointer");
+        return nullptr;
+    }
+    const size_t ngroups = (size_t)N * (K / kGroup);
+    if (check_scales(scales, ngroups) != QLIN_OK) return nullptr;
+    if (!symmetric && check_zeros(zeros, ngroups) != QLIN_OK) return nullptr;
+
+    qlin_s *h = new qlin_s;
+    h->K = K;
+    h->N = N;
+    h->Kb = (int)(K / kGroup);
+    h->Nt = (int)(N / kTileN);
+    h->symmetric = symmetric;
+    const size_t code_bytes = (size_t)N * K / 2;
+    const size_t sz_bytes = ngroups * (symmetric ? 2 : 4);
+    h->counters_n = std::max(h->Nt, 1);
+    // rows of partial sums the smallest feasible K split needs for each m-tile count
+    h->ws_rows = kWsRowsMin;
+    for (int mt = 1; mt <= kMaxSkinnyM / 16; ++mt) {
+        const int kc_max = (int)(kXLdsBudget / ((size_t)16 * mt * 256));
+        const int s_min = (h->Kb + kc_max - 1) / kc_max;
+        if (s_min > 1) h->ws_rows = std::max(h->ws_rows, s_min * 16 * mt);
+    }
+
+    void *canon = nullptr, *sc = nullptr, *zc = nullptr;
+    hipError_t e = hipSuccess;
+    auto bail = [&](const char *what, hipError_t e) -> qlin_t {
+        if (e == hipErrorOutOfMemory) fail(QLIN_ERR_OOM, "device allocation failed (%s)", what);
+        else hip_fail(e, what);
+        if (canon) (void)hipFree(canon);
+        if (sc) (void)hipFree(sc);
+        if (zc) (void)hipFree(zc);
+        free_handle(h);
+        return nullptr;
+    };
+    if ((e = dev_alloc((void **)&h->codes, code_bytes)) != hipSuccess) return bail("codes", e);
+    if ((e = dev_alloc(&h->sz, sz_bytes)) != hipSuccess) return bail("scales", e);
+    if ((e = dev_alloc((void **)&h->ws, (size_t)h->ws_rows * N * 4)) != hipSuccess) return bail("workspace", e);
+    if ((e = dev_alloc((void **)&h->counters, (size_t)h->counters_n * 4)) != hipSuccess) return bail("counters", e);
+    if ((e = dev_alloc(&canon, code_bytes)) != hipSuccess) return bail("staging", e);
+    if ((e = dev_alloc(&sc, ngroups * 2)) != hipSuccess) return bail("staging", e);
+    if (!symmetric && (e = dev_alloc(&zc, ngroups * 2)) != hipSuccess) return bail("staging", e);
+
+    if ((e = hipGetDevice(&h->device)) != hipSuccess) return bail("hipGetDevice", e);
+    if ((e = hipDeviceGetAttribute(&h->num_cu, hipDeviceAttributeMultiprocessorCount, h->device)) != hipSuccess)
+        return bail("hipDeviceGetAttribute", e);
+    static std::once_flag once;
+    std::call_once(once, [] { (void)prepare_kernels(); (void)hipGetLastError(); });
+    if ((e = hipMemcpy(canon, packed, code_bytes, hipMemcpyHostToDevice)) != hipSuccess)
+        return bail("copy codes", e);
+    if ((e = hipMemcpy(sc, scales, ngroups * 2, hipMemcpyHostToDevice)) != hipSuccess)
+        return bail("copy scales", e);
+    if (!symmetric && (e = hipMemcpy(zc, zeros, ngroups * 2, hipMemcpyHostToDevice)) != hipSuccess)
+        return bail("copy zeros", e);
+    if ((e = hipMemset(h->counters, 0, (size_t)h->counters_n * 4)) != hipSuccess)
+        return bail("hipMemset", e);
+    if ((e = launch_repack((const uint32_t *)canon, (const uint16_t *)sc, (const uint16_t *)zc, h->codes, h->sz,
+                           (int)K, (int)N, symmetric, nullptr)) != hipSuccess)
+        return bail("repack launch", e);
+    if ((e = hipDeviceSynchronize()) != hipSuccess) return bail("repack", e);
+    (void)hipFree(canon);
+    (void)hipFree(sc);
+    if (zc) (void)hipFree(zc);
+    return h;
+}
+
+// ------------------------------------------------------------------ planning
+
+struct Plan {
+    int path = 0;
+    int mrows = 0;     // template row count (GEMV: M; SKINNY: 16 * m-tiles)
+    int S = 1, Gn = 1, grid = 1;
+    size_t lds = 0;
+};
+
+// Auto M-dispatch: vector-ALU GEMV up to this M, matrix-core SKINNY above.
+int gemv_max_auto() {
+    static int v = [] {
+        const char *e = getenv("QLIN_GEMV_MAX_M");
+        return e ? std::max(0, std::min(kMaxGemvM, atoi(e))) : 2;
+    }();
+    return v;
+}
+
+// Cost (ns) of a (S, Gn) split: the slowest workgroup's share of HBM time,
+// the activation staging it does first, and the partial-sum traffic + arrival
+// fix-up when the K range is cut (S > 1).
+double plan_cost(const qlin_s *h, int path, int mrows, int M, int S, int Gn) {
+    const double bw = 6.0e3;                          // bytes per ns, sustained HBM read
+    const double per_cu = bw / h->num_cu;
+    const int Kc = (h->Kb + S - 1) / S, Tn = (h->Nt + Gn - 1) / Gn;
+    const int G = S * Gn;
+    const int rounds = (G + h->num_cu - 1) / h->num_cu;
+    const double blk = 1024.0 + (h->symmetric ? 32.0 : 64.0);
+    const double wg_bytes = (double)Tn * Kc * blk;
+    double t = std::max(rounds * wg_bytes / per_cu, (double)h->Nt * h->Kb * blk / bw);
+    const int xrows = (path == kGemv) ? M : mrows;
+    t += rounds * (double)Kc * xrows * 256.0 / 100.0;   // ~100 B/ns per CU from L2 into LDS
+    if (S > 1) t += 2.0 * S * M * (double)h->N * 4.0 / bw + 1500.0;
+    return t;
+}
+
+int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
+    if (path == kAuto) path = (M <= gemv_max_auto()) ? kGemv : kSkinny;
+    if (path == kTiled) path = kSkinny;   // prefill-sized M is run in 64-row slices for now
+    if (path != kGemv && path != kSkinny) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
+    if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= 8");
+    const int Mi = (int)std::min<int64_t>(M, kMaxSkinnyM);
+    p->path = path;
+    p->mrows = (path == kGemv) ? Mi : 16 * ((Mi + 15) / 16);
+    const int rows = p->mrows;
+    if (split_k < 0 || split_k > h->Kb) return fail(QLIN_ERR_INVALID, "split_k must be in [0, K/128]");
+
+    auto fits = [&](int S, int Gn) {
+        const int Kc = (h->Kb + S - 1) / S, Tn = (h->Nt + Gn - 1) / Gn;
+        if (S > 1 && S * Mi > h->ws_rows) return false;
+        if (Gn > h->counters_n) return false;
+        return lds_bytes(path, rows, Kc, Tn) <= kLdsMax;
+    };
+    auto gn_for = [&](int S) { return std::max(1, std::min(h->Nt, (int)std::lround((double)h->num_cu / S))); };
+
+    int bestS = -1, bestGn = 1;
+    if (split_k > 0) {
+        const int S = (int)split_k;
+        int Gn = gn_for(S);
+        while (Gn < h->Nt && !fits(S, Gn)) ++Gn;
+        if (!fits(S, Gn)) return fail(QLIN_ERR_UNSUPPORTED, "split_k=%d does not fit (LDS or workspace)", S);
+        bestS = S;
+        bestGn = Gn;
+    } else {
+        double best = 1e300;
+        for (int S = 1; S <= std::min(h->Kb, 64); ++S) {
+            int Gn = gn_for(S);
+            while (Gn < h->Nt && !fits(S, Gn)) ++Gn;
+            if (!fits(S, Gn)) continue;
+            const double c = plan_cost(h, path, rows, Mi, S, Gn);
+            if (c < best) { best = c; bestS = S; bestGn = Gn; }
+        }
+        if (bestS < 0) return fail(QLIN_ERR_UNSUPPORTED, "no work split fits this shape");
+    }
+    p->S = bestS;
+    p->Gn = bestGn;
+    p->grid = bestS * bestGn;
+    const int Kc = (h->Kb + bestS - 1) / bestS, Tn = (h->Nt + bestGn - 1) / bestGn;
+    // at least 80 KiB + 1 of LDS per workgroup keeps one workgroup per CU, so
+    // the grid spreads over all CUs
+    p->lds = std::max(lds_bytes(path, rows, Kc, Tn), (size_t)80 * 1024 + 256);
+    return QLIN_OK;
+}
+
+int check_forward_args(const qlin_s *h, int64_t M, const uint16_t *x, const uint16_t *y) {
+    if (!h) return fail(QLIN_ERR_INVALID, "NULL handle");
+    if (M < 0) return fail(QLIN_ERR_INVALID, "M must be >= 0");
+    if (M == 0) return QLIN_OK;
+    if (M > kMaxM) return fail(QLIN_ERR_UNSUPPORTED, "M must be <= 65536");
+    if (!x || !y) return fail(QLIN_ERR_INVALID, "NULL x or y");
+    if (((uintptr_t)x | (uintptr_t)y) & 15) return fail(QLIN_ERR_ALIGN, "x and y must be 16-byte aligned");
+    const uintptr_t xa = (uintptr_t)x, xe = xa + (uintptr_t)(M * h->K * 2);
+    const uintptr_t ya = (uintptr_t)y, ye = ya + (uintptr_t)(M * h->N * 2);
+    if (xa < ye && ya < xe) return fail(QLIN_ERR_INVALID, "y overlaps x");
+    return QLIN_OK;
+}
+
+int run_forward(qlin_s *h, int path, int64_t split_k, int64_t M, const uint16_t *x, uint16_t *y, void *stream) {
+    clear_err();
+    int rc = check_forward_args(h, M, x, y);
+    if (rc != QLIN_OK || M == 0) return rc;
+    if (path == kSkinny && M > kMaxSkinnyM) return fail(QLIN_ERR_UNSUPPORTED, "SKINNY path needs M <= 64");
+    if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= 8");
+    if (path < kAuto || path > kTiled) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != h->device) return fail(QLIN_ERR_INVALID, "handle belongs to device %d, current is %d", h->device, dev);
+    hipStream_t st = (hipStream_t)stream;
+    // rows beyond 64 run as consecutive 64-row slices
+    for (int64_t m0 = 0; m0 < M; m0 += kMaxSkinnyM) {
+        const int64_t Ms = std::min<int64_t>(kMaxSkinnyM, M - m0);
+        Plan p;
+        rc = make_plan(h, path, split_k, Ms, &p);
+        if (rc != QLIN_OK) return rc;
+        FwdArgs a;
+        a.codes = h->codes;
+        a.sz = h->sz;
+        a.x = x + m0 * h->K;
+        a.y = y + m0 * h->N;
+        a.ws = h->ws;
+        a.counters = h->counters;
+        a.M = (int)Ms;
+        a.K = (int)h->K;
+        a.N = (int)h->N;
+        a.Kb = h->Kb;
+        a.Nt = h->Nt;
+        a.S = p.S;
+        a.Gn = p.Gn;
+        e = launch_forward(p.path, p.mrows, h->symmetric, p.grid, p.lds, a, st);
+        if (e != hipSuccess) return hip_fail(e, "forward launch");
+    }
+    return QLIN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+qlin_t qlin_create(int64_t K, int64_t N, int64_t group, const uint32_t *packed_w, const uint16_t *scales,
+                   const uint16_t *zeros) {
+    return create_impl(K, N, group, packed_w, scales, zeros, false);
+}
+
+qlin_t qlin_create_symmetric(int64_t K, int64_t N, int64_t group, const uint32_t *packed_w,
+                             const uint16_t *scales) {
+    return create_impl(K, N, group, packed_w, scales, nullptr, true);
+}
+
+int qlin_forward(qlin_t h, int64_t M, const uint16_t *x, uint16_t *y, void *stream) {
+    return run_forward(h, kAuto, 0, M, x, y, stream);
+}
+
+int qlin_forward_path(qlin_t h, int path, int64_t split_k, int64_t M, const uint16_t *x, uint16_t *y,
+                      void *stream) {
+    if (h && (split_k < 0 || split_k > h->Kb)) {
+        clear_err();
+        return fail(QLIN_ERR_INVALID, "split_k must be in [0, K/128]");
+    }
+    return run_forward(h, path, split_k, M, x, y, stream);
+}
+
+int qlin_plan(qlin_t h, int path, int64_t split_k, int64_t M, char *buf, int64_t buflen) {
+    clear_err();
+    if (!h) return fail(QLIN_ERR_INVALID, "NULL handle");
+    if (!buf || buflen <= 0) return fail(QLIN_ERR_INVALID, "NULL buffer");
+    if (M <= 0 || M > kMaxM) return fail(QLIN_ERR_INVALID, "M must be in [1, 65536]");
+    if (path < kAuto || path > kTiled) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
+    if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= 8");
+    if (path == kSkinny && M > kMaxSkinnyM) return fail(QLIN_ERR_UNSUPPORTED, "SKINNY path needs M <= 64");
+    Plan p;
+    int rc = make_plan(h, path, split_k, std::min<int64_t>(M, kMaxSkinnyM), &p);
+    if (rc != QLIN_OK) return rc;
+    const int64_t slices = (M + kMaxSkinnyM - 1) / kMaxSkinnyM;
+    snprintf(buf, (size_t)buflen, "path=%s kernel=%s grid=%d block=%d split=%d ranges=%d lds=%zu launches=%lld",
+             p.path == kGemv ? "gemv" : "skinny", kernel_name(p.path, p.mrows, h->symmetric), p.grid, kThreads,
+             p.S, p.Gn, p.lds, (long long)slices);
+    return QLIN_OK;
+}
+
+void qlin_destroy(qlin_t h) {
+    if (!h) return;
+    int prev = -1;
+    if (hipGetDevice(&prev) == hipSuccess && prev != h->device && hipSetDevice(h->device) == hipSuccess) {
+        (void)hipDeviceSynchronize();
+        free_handle(h);
+        (void)hipSetDevice(prev);
+        return;
+    }
+    (void)hipDeviceSynchronize();
+    free_handle(h);
+}
+
+const char *qlin_last_error(void) { return g_err; }
+
+int qlin_last_status(void) { return g_status; }
+
+int qlin_unpack_codes(qlin_t h, uint8_t *q_out, void *stream) {
+    clear_err();
+    if (!h || !q_out) return fail(QLIN_ERR_INVALID, "NULL argument");
+    if ((uintptr_t)q_out & 15) return fail(QLIN_ERR_ALIGN, "q_out must be 16-byte aligned");
+    hipError_t e = launch_unpack(h->codes, q_out, (int)h->K, (int)h->N, (hipStream_t)stream);
+    return e == hipSuccess ? QLIN_OK : hip_fail(e, "unpack launch");
+}
+
+int qlin_dequantize(qlin_t h, int routine, uint16_t *w_out, void *stream) {
+    clear_err();
+    if (!h || !w_out) return fail(QLIN_ERR_INVALID, "NULL argument");
+    if (routine != 0 && routine != 1) return fail(QLIN_ERR_INVALID, "routine must be 0 or 1");
+    if ((uintptr_t)w_out & 15) return fail(QLIN_ERR_ALIGN, "w_out must be 16-byte aligned");
+    hipError_t e = launch_dequant(routine, h->codes, h->sz, h->symmetric, w_out, (int)h->K, (int)h->N,
+                                  (hipStream_t)stream);
+    return e == hipSuccess ? QLIN_OK : hip_fail(e, "dequantize launch");
+}
+
+int qlin_shape(qlin_t h, int64_t *K, int64_t *N) {
+    clear_err();
+    if (!h) return fail(QLIN_ERR_INVALID, "NULL handle");
+    if (K) *K = h->K;
+    if (N) *N = h->N;
+    return QLIN_OK;
+}
+
+}  // extern "C"

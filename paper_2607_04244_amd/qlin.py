@@ -1,0 +1,212 @@
+"""Python binding of ``libqlin.so`` (argument marshalling only).
+
+The functions mirror the C ABI in ``include/qlin.h`` one to one; ``QLinear``
+wraps a handle for torch callers.  torch supplies device memory and the
+current stream; every step of the computation runs in the HIP kernels.  The
+module raises if the library has not been built - there is no fallback.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libqlin.so")
+
+QLIN_OK = 0
+QLIN_ERR_INVALID = -1
+QLIN_ERR_UNSUPPORTED = -2
+QLIN_ERR_ALIGN = -3
+QLIN_ERR_OOM = -4
+QLIN_ERR_HIP = -5
+
+PATH_AUTO, PATH_GEMV, PATH_SKINNY, PATH_TILED = 0, 1, 2, 3
+
+# every symbol include/qlin.h declares
+EXPORTS = ("qlin_create", "qlin_create_symmetric", "qlin_forward", "qlin_forward_path",
+           "qlin_plan", "qlin_destroy", "qlin_last_error", "qlin_unpack_codes",
+           "qlin_dequantize", "qlin_shape", "qlin_last_status")
+
+_lib = None
+
+
+class QlinError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"qlin error {code}: {msg}")
+        self.code = code
+
+
+def lib():
+    """Load ``libqlin.so`` (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"HIP library {LIB_PATH} is missing: run __graft_entry__.build() first")
+    L = ctypes.CDLL(LIB_PATH)
+    P, I64, I32, VP = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p
+    L.qlin_create.restype = P
+    L.qlin_create.argtypes = [I64, I64, I64, VP, VP, VP]
+    L.qlin_create_symmetric.restype = P
+    L.qlin_create_symmetric.argtypes = [I64, I64, I64, VP, VP]
+    L.qlin_forward.restype = I32
+    L.qlin_forward.argtypes = [P, I64, VP, VP, VP]
+    L.qlin_forward_path.restype = I32
+    L.qlin_forward_path.argtypes = [P, I32, I64, I64, VP, VP, VP]
+    L.qlin_plan.restype = I32
+    L.qlin_plan.argtypes = [P, I32, I64, I64, ctypes.c_char_p, I64]
+    L.qlin_destroy.restype = None
+    L.qlin_destroy.argtypes = [P]
+    L.qlin_last_error.restype = ctypes.c_char_p
+    L.qlin_last_error.argtypes = []
+    L.qlin_last_status.restype = I32
+    L.qlin_last_status.argtypes = []
+    L.qlin_unpack_codes.restype = I32
+    L.qlin_unpack_codes.argtypes = [P, VP, VP]
+    L.qlin_dequantize.restype = I32
+    L.qlin_dequantize.argtypes = [P, I32, VP, VP]
+    L.qlin_shape.restype = I32
+    L.qlin_shape.argtypes = [P, ctypes.POINTER(I64), ctypes.POINTER(I64)]
+    _lib = L
+    return L
+
+
+def last_error():
+    return lib().qlin_last_error().decode()
+
+
+def qlin_last_error():
+    return last_error()
+
+
+def qlin_last_status():
+    return lib().qlin_last_status()
+
+
+def _check(rc):
+    if rc != QLIN_OK:
+        raise QlinError(rc, last_error())
+    return rc
+
+
+def _host_ptr(a, dtype):
+    if a is None:
+        return None, None
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data
+
+
+# ---------------------------------------------------------------- C ABI mirror
+
+def qlin_create(K, N, group, packed_w, scales, zeros):
+    """Host numpy arrays in; returns the handle (int) or raises QlinError."""
+    p, pp = _host_ptr(packed_w, np.uint32)
+    s, sp = _host_ptr(scales, np.uint16)
+    z, zp = _host_ptr(zeros, np.uint16)
+    h = lib().qlin_create(K, N, group, pp, sp, zp)
+    if not h:
+        raise QlinError(lib().qlin_last_status(), last_error())
+    return h
+
+
+def qlin_create_symmetric(K, N, group, packed_w, scales):
+    p, pp = _host_ptr(packed_w, np.uint32)
+    s, sp = _host_ptr(scales, np.uint16)
+    h = lib().qlin_create_symmetric(K, N, group, pp, sp)
+    if not h:
+        raise QlinError(lib().qlin_last_status(), last_error())
+    return h
+
+
+def qlin_forward(h, M, x_ptr, y_ptr, stream):
+    return lib().qlin_forward(h, M, x_ptr, y_ptr, stream)
+
+
+def qlin_forward_path(h, path, split_k, M, x_ptr, y_ptr, stream):
+    return lib().qlin_forward_path(h, path, split_k, M, x_ptr, y_ptr, stream)
+
+
+def qlin_plan(h, path, split_k, M):
+    buf = ctypes.create_string_buffer(256)
+    _check(lib().qlin_plan(h, path, split_k, M, buf, len(buf)))
+    return buf.value.decode()
+
+
+def qlin_destroy(h):
+    lib().qlin_destroy(h)
+
+
+def qlin_unpack_codes(h, q_ptr, stream):
+    return lib().qlin_unpack_codes(h, q_ptr, stream)
+
+
+def qlin_dequantize(h, routine, w_ptr, stream):
+    return lib().qlin_dequantize(h, routine, w_ptr, stream)
+
+
+def qlin_shape(h):
+    K, N = ctypes.c_int64(), ctypes.c_int64()
+    _check(lib().qlin_shape(h, ctypes.byref(K), ctypes.byref(N)))
+    return K.value, N.value
+
+
+# ---------------------------------------------------------------- torch wrapper
+
+class QLinear:
+    """One W4A16 linear layer on the current GPU.
+
+    ``packed``/``scales``/``zeros`` are host arrays in the canonical layout
+    (see include/qlin.h); ``zeros=None`` selects the symmetric format.
+    """
+
+    def __init__(self, packed, scales, zeros=None, group=128):
+        packed = np.asarray(packed)
+        self.N, K8 = packed.shape
+        self.K = K8 * 8
+        if zeros is None:
+            self.h = qlin_create_symmetric(self.K, self.N, group, packed, scales)
+        else:
+            self.h = qlin_create(self.K, self.N, group, packed, scales, zeros)
+
+    def _stream(self):
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+
+    def forward(self, x, out=None, path=PATH_AUTO, split_k=0):
+        import torch
+        if x.dtype != torch.bfloat16 or not x.is_cuda or x.dim() != 2 or x.shape[1] != self.K:
+            raise ValueError("x must be a CUDA bf16 tensor of shape [M, K]")
+        x = x.contiguous()
+        M = x.shape[0]
+        y = out if out is not None else torch.empty((M, self.N), dtype=torch.bfloat16, device=x.device)
+        _check(qlin_forward_path(self.h, path, split_k, M, x.data_ptr(), y.data_ptr(), self._stream()))
+        return y
+
+    __call__ = forward
+
+    def plan(self, M, path=PATH_AUTO, split_k=0):
+        return qlin_plan(self.h, path, split_k, M)
+
+    def unpack_codes(self):
+        import torch
+        q = torch.empty((self.N, self.K), dtype=torch.uint8, device="cuda")
+        _check(qlin_unpack_codes(self.h, q.data_ptr(), self._stream()))
+        return q
+
+    def dequantize(self, routine=0):
+        import torch
+        w = torch.empty((self.N, self.K), dtype=torch.bfloat16, device="cuda")
+        _check(qlin_dequantize(self.h, routine, w.data_ptr(), self._stream()))
+        return w
+
+    def close(self):
+        if getattr(self, "h", None):
+            qlin_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,135 @@
+"""The C ABI library loads, exports what include/qlin.h declares, and rejects
+bad arguments before any HIP call (CPU only: no compute is launched)."""
+
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2607_04244_amd import qlin
+from synth import gen
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    txt = open(os.path.join(ROOT, "include", "qlin.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(qlin_[a-z_]+)\s*\(", txt)))
+
+
+def test_header_declares_the_binding_names():
+    assert _declared_functions() == sorted(qlin.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = qlin.lib()
+    for name in _declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_missing_library_fails_loudly(monkeypatch, tmp_path):
+    monkeypatch.setattr(qlin, "_lib", None)
+    monkeypatch.setattr(qlin, "LIB_PATH", str(tmp_path / "absent.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        qlin.lib()
+
+
+@pytest.fixture(scope="module")
+def case():
+    return gen.random_case(1, 1, 256, 32)
+
+
+def _create_code(K, N, group, packed, scales, zeros, symmetric=False):
+    try:
+        if symmetric:
+            qlin.qlin_create_symmetric(K, N, group, packed, scales)
+        else:
+            qlin.qlin_create(K, N, group, packed, scales, zeros)
+    except qlin.QlinError as e:
+        return e.code
+    raise AssertionError("create unexpectedly succeeded")
+
+
+@pytest.mark.parametrize("K,N,group,code", [
+    (0, 32, 128, qlin.QLIN_ERR_INVALID),
+    (256, 0, 128, qlin.QLIN_ERR_INVALID),
+    (256, 32, 0, qlin.QLIN_ERR_INVALID),
+    (256, 32, 64, qlin.QLIN_ERR_UNSUPPORTED),
+    (200, 32, 128, qlin.QLIN_ERR_INVALID),
+    (256, 24, 128, qlin.QLIN_ERR_UNSUPPORTED),
+    (65536 + 128, 32, 128, qlin.QLIN_ERR_UNSUPPORTED),
+])
+def test_create_rejects_bad_shapes(case, K, N, group, code):
+    assert _create_code(K, N, group, case["packed"], case["scales"], case["zeros"]) == code
+
+
+def test_create_rejects_null_pointers(case):
+    L = qlin.lib()
+    p = case["packed"]
+    s = case["scales"]
+    assert not L.qlin_create(256, 32, 128, None, s.ctypes.data, s.ctypes.data)
+    assert qlin.qlin_last_status() == qlin.QLIN_ERR_INVALID
+    assert not L.qlin_create(256, 32, 128, p.ctypes.data, None, s.ctypes.data)
+    assert qlin.qlin_last_status() == qlin.QLIN_ERR_INVALID
+    assert not L.qlin_create(256, 32, 128, p.ctypes.data, s.ctypes.data, None)
+    assert qlin.qlin_last_status() == qlin.QLIN_ERR_INVALID
+    assert not L.qlin_create_symmetric(256, 32, 128, p.ctypes.data, None)
+    assert qlin.qlin_last_status() == qlin.QLIN_ERR_INVALID
+
+
+@pytest.mark.parametrize("zbits", [0x40F0, 0x4180, 0xBF80, 0x7FC0, 0x3F00])   # 7.5, 16, -1, nan, 0.5
+def test_create_rejects_non_integer_or_out_of_range_zeros(case, zbits):
+    z = case["zeros"].copy()
+    z[5, 1] = zbits
+    assert _create_code(256, 32, 128, case["packed"], case["scales"], z) == qlin.QLIN_ERR_INVALID
+    assert "zero-point" in qlin.last_error()
+
+
+@pytest.mark.parametrize("sbits", [0x0000, 0x8000, 0xBC00, 0x7F80, 0x7FC0, 0x0001, 0x0D00, 0x7300])
+def test_create_rejects_scales_outside_the_exact_range(case, sbits):
+    # zero, -0, negative, inf, nan, denormal, 2^-101, 2^103
+    s = case["scales"].copy()
+    s[3, 0] = sbits
+    assert _create_code(256, 32, 128, case["packed"], s, case["zeros"]) == qlin.QLIN_ERR_UNSUPPORTED
+    assert _create_code(256, 32, 128, case["packed"], s, None, symmetric=True) == qlin.QLIN_ERR_UNSUPPORTED
+
+
+def test_scale_range_edges_pass_validation(case, monkeypatch):
+    # 2^-100 and the largest value below 2^100 are accepted: validation passes
+    # and the forced allocation failure is reported instead
+    monkeypatch.setenv("QLIN_FAULT", "alloc")
+    s = case["scales"].copy()
+    s[0, 0] = (127 - 100) << 7
+    s[0, 1] = ((127 + 99) << 7) | 0x7F
+    assert _create_code(256, 32, 128, case["packed"], s, case["zeros"]) == qlin.QLIN_ERR_OOM
+
+
+def test_allocation_failure_is_reported_not_aborted(case, monkeypatch):
+    monkeypatch.setenv("QLIN_FAULT", "alloc")
+    assert _create_code(256, 32, 128, case["packed"], case["scales"], case["zeros"]) == qlin.QLIN_ERR_OOM
+    assert "allocation failed" in qlin.last_error()
+    assert _create_code(256, 32, 128, case["packed"], case["scales"], None, symmetric=True) == qlin.QLIN_ERR_OOM
+
+
+def test_calls_on_a_null_handle():
+    L = qlin.lib()
+    assert L.qlin_forward(None, 1, 16, 32, None) == qlin.QLIN_ERR_INVALID
+    assert L.qlin_forward_path(None, 2, 0, 1, 16, 32, None) == qlin.QLIN_ERR_INVALID
+    assert L.qlin_unpack_codes(None, 16, None) == qlin.QLIN_ERR_INVALID
+    assert L.qlin_dequantize(None, 0, 16, None) == qlin.QLIN_ERR_INVALID
+    assert L.qlin_shape(None, None, None) == qlin.QLIN_ERR_INVALID
+    buf = qlin.ctypes.create_string_buffer(64)
+    assert L.qlin_plan(None, 0, 0, 1, buf, 64) == qlin.QLIN_ERR_INVALID
+    L.qlin_destroy(None)                       # NULL-safe
+    assert qlin.qlin_last_status() == qlin.QLIN_ERR_INVALID
+    assert "NULL" in qlin.last_error()
+
+
+def test_error_state_is_cleared_by_the_next_call(case, monkeypatch):
+    monkeypatch.setenv("QLIN_FAULT", "alloc")
+    _create_code(0, 32, 128, case["packed"], case["scales"], case["zeros"])
+    assert qlin.qlin_last_status() == qlin.QLIN_ERR_INVALID
+    _create_code(256, 32, 128, case["packed"], case["scales"], case["zeros"])
+    assert qlin.qlin_last_status() == qlin.QLIN_ERR_OOM
