@@ -8,14 +8,17 @@
 // Device weight layout ("block layout").  The canonical [N][K/8] words are
 // re-laid-out at handle creation into blocks of 16 columns x 128 k (one
 // quantization group of one column tile) = 256 words = 1 KiB.  Block (t, kb)
-// starts at word (t * Kb + kb) * 256, so a wave that walks the groups of one
-// column tile reads consecutive KiB.  Lane l of a wave owns words
+// starts at word (kb * Nt + t) * 256 (Nt = N / 16 tiles): the blocks of one
+// group for consecutive column tiles are consecutive KiB, which is the order
+// the forward kernels stream them in.  Lane l of a wave owns words
 // [4l, 4l + 4) of a block (one 128-bit load); word j of lane l covers k in
 // [32j, 32j + 32) of the group, and its nibble p holds the code of
 //     n = 16 t + 4 * ((l >> 2) & 3) + r,   r  = 2 * (p & 1) + (p >> 2)
-//     k = 128 kb + 32 j + 16 h + 4 * (l >> 4) + (l & 3),   h = (p >> 1) & 1.
+//     k = 128 kb + 32 j + 8 * (l >> 4) + 4 h + (l & 3),   h = (p >> 1) & 1.
 // That is exactly the operand order of the dequantizing matrix op below, so
-// no lane shuffle is needed between HBM and the MFMA.
+// no lane shuffle is needed between HBM and the MFMA, and each lane ends up
+// with 8 consecutive k of one column: its x operand is one contiguous
+// 16-byte piece of x.
 //
 // Dequantization on the matrix cores.  For nibble pairs extracted as bf16
 // "128 + q" (bit trick: 0x4300 | q is bf16 128 + q), one
@@ -28,6 +31,8 @@
 // to the definition; the unpack/dequantize test hooks check that.
 
 #include "qlin_internal.h"
+
+#include <cstdio>
 
 namespace qlin {
 
@@ -46,7 +51,7 @@ __host__ __device__ inline void block_coord(int l, int j, int p, int &n16, int &
     const int r = 2 * (p & 1) + (p >> 2);
     const int h = (p >> 1) & 1;
     n16 = 4 * ((l >> 2) & 3) + r;
-    k128 = 32 * j + 16 * h + 4 * (l >> 4) + (l & 3);
+    k128 = 32 * j + 8 * (l >> 4) + 4 * h + (l & 3);
 }
 
 // ------------------------------------------------------------------ small helpers
@@ -66,17 +71,30 @@ __device__ inline float bf16_lo_to_f32(uint32_t w) { return __uint_as_float(w <<
 __device__ inline float bf16_hi_to_f32(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // The four "128 + q" bf16 pairs of one packed word: pair i holds nibbles i
-// (low half) and i + 4 (high half).
+// (low half) and i + 4 (high half).  Each pair is one v_and_or_b32; the two
+// constants live in registers (gfx9 VOP3 takes no literal), loaded once per
+// kernel by ExtractConsts.
+struct ExtractConsts {
+    uint32_t mask, magic;
+    __device__ inline ExtractConsts() {
+        // opaque to the optimizer, so the values stay in registers
+        mask = __builtin_amdgcn_readfirstlane(0x000F000Fu);
+        magic = 0x43004300u;                        // bf16 128.0 in both halves
+        asm volatile("" : "+v"(magic));
+    }
+};
 struct Pairs { uint32_t a0, a1, a2, a3; };
-__device__ inline Pairs extract_pairs(uint32_t P) {
-    constexpr uint32_t kMask = 0x000F000Fu, kMagic = 0x43004300u;   // bf16 128.0 in both halves
+__device__ inline Pairs extract_pairs(uint32_t P, const ExtractConsts &k) {
     Pairs o;
-    o.a0 = (P & kMask) | kMagic;
-    o.a1 = ((P >> 4) & kMask) | kMagic;
-    o.a2 = ((P >> 8) & kMask) | kMagic;
-    o.a3 = ((P >> 12) & kMask) | kMagic;
+    o.a0 = (P & k.mask) | k.magic;
+    o.a1 = ((P >> 4) & k.mask) | k.magic;
+    o.a2 = ((P >> 8) & k.mask) | k.magic;
+    o.a3 = ((P >> 12) & k.mask) | k.magic;
     return o;
 }
+
+// One lane's 16 bytes of a weight block.
+__device__ inline uint4 load_block(const uint4 *codes, size_t idx) { return codes[idx]; }
 
 // s | z << 16 word of a column (symmetric handles store only s; z = 8).
 template <bool SYM>
@@ -108,10 +126,10 @@ __device__ inline MfmaDeq mfma_setup(uint32_t sz, uint32_t shift, uint32_t keep_
 }
 
 // Dequantize one packed word into the 8 bf16 A-operand values of
-// v_mfma_f32_16x16x32_bf16 (row n = l & 15): elements e = 4h + i hold
-// w[n][32j + 16h + 4(l >> 4) + i].
-__device__ inline v8bf mfma_dequant(uint32_t P, const MfmaDeq &d) {
-    const Pairs a = extract_pairs(P);
+// v_mfma_f32_16x16x32_bf16 (row n = l & 15): element e holds
+// w[n][32j + 8(l >> 4) + e].
+__device__ inline v8bf mfma_dequant(uint32_t P, const MfmaDeq &d, const ExtractConsts &k) {
+    const Pairs a = extract_pairs(P, k);
     const v4s A0 = __builtin_bit_cast(v4s, v2u{a.a0, a.a1});
     const v4s A1 = __builtin_bit_cast(v4s, v2u{a.a2, a.a3});
     const v4f d0 = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(A0, d.bdiag, d.c4, 0, 0, 0);
@@ -143,10 +161,10 @@ __device__ inline float dot2(uint32_t a, uint32_t b, float c) {
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(v2bf, a), __builtin_bit_cast(v2bf, b), c, false);
 }
 
-// Dequantize one packed word: pr[r] = bf16 pair (w[n_r][k0], w[n_r][k0 + 16]) with
-// k0 = 32j + 4(l >> 4) + (l & 3).
-__device__ inline void valu_dequant(uint32_t P, const ValuDeq &d, uint32_t pr[4]) {
-    const Pairs a = extract_pairs(P);
+// Dequantize one packed word: pr[r] = bf16 pair (w[n_r][k0], w[n_r][k0 + 4]) with
+// k0 = 32j + 8(l >> 4) + (l & 3).
+__device__ inline void valu_dequant(uint32_t P, const ValuDeq &d, const ExtractConsts &k, uint32_t pr[4]) {
+    const Pairs a = extract_pairs(P, k);
     const float w00 = dot2(a.a0, d.sl[0], d.c[0]), w01 = dot2(a.a0, d.sh[1], d.c[1]);
     const float w02 = dot2(a.a1, d.sl[2], d.c[2]), w03 = dot2(a.a1, d.sh[3], d.c[3]);
     const float w10 = dot2(a.a2, d.sl[0], d.c[0]), w11 = dot2(a.a2, d.sh[1], d.c[1]);
@@ -168,7 +186,8 @@ __global__ void k_repack_codes(const uint32_t *__restrict__ canon, uint32_t *__r
         const size_t b = idx / kBlockU32;
         const int within = (int)(idx % kBlockU32);
         const int l = within >> 2, j = within & 3;
-        const int t = (int)(b / Kb), kb = (int)(b % Kb);
+        const int Nt = N / kTileN;
+        const int kb = (int)(b / Nt), t = (int)(b % Nt);
         uint32_t word = 0;
         for (int p = 0; p < 8; ++p) {
             int n16, k128;
@@ -188,8 +207,9 @@ __global__ void k_repack_sz(const uint16_t *__restrict__ scales, const uint16_t 
     for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
          idx += (size_t)gridDim.x * blockDim.x) {
         const int n16 = (int)(idx % kTileN);
-        const size_t tb = idx / kTileN;               // t * Kb + kb
-        const int kb = (int)(tb % Kb), t = (int)(tb / Kb);
+        const size_t tb = idx / kTileN;               // kb * Nt + t
+        const int Nt = N / kTileN;
+        const int kb = (int)(tb / Nt), t = (int)(tb % Nt);
         const size_t n = (size_t)t * kTileN + n16;
         const uint16_t s = scales[n * Kb + kb];
         if (symmetric) {
@@ -210,7 +230,7 @@ __global__ void k_unpack(const uint4 *__restrict__ codes, uint8_t *__restrict__ 
          b += (size_t)gridDim.x * (blockDim.x >> 6)) {
         const uint4 c = codes[b * 64 + l];
         const uint32_t w[4] = {c.x, c.y, c.z, c.w};
-        const int t = (int)(b / Kb), kb = (int)(b % Kb);
+        const int kb = (int)(b / (N / kTileN)), t = (int)(b % (N / kTileN));
         for (int j = 0; j < 4; ++j)
             for (int p = 0; p < 8; ++p) {
                 int n16, k128;
@@ -227,19 +247,20 @@ __global__ void k_dequant_mfma(const uint4 *__restrict__ codes, const void *__re
     const size_t nblocks = (size_t)(N / kTileN) * Kb;
     const int l = threadIdx.x & 63;
     const uint32_t shift = (l & 1) * 16, keep_lo = (l & 2) ? 0u : 0xFFFFFFFFu;
+    const ExtractConsts kx;
     for (size_t b = (size_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); b < nblocks;
          b += (size_t)gridDim.x * (blockDim.x >> 6)) {
         const uint4 c = codes[b * 64 + l];
         const MfmaDeq d = mfma_setup(load_sz<SYM>(sz, b * kTileN + (l & 15)), shift, keep_lo);
         const uint32_t P[4] = {c.x, c.y, c.z, c.w};
-        const int t = (int)(b / Kb), kb = (int)(b % Kb);
+        const int kb = (int)(b / (N / kTileN)), t = (int)(b % (N / kTileN));
         const size_t n = (size_t)t * kTileN + (l & 15);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const v4u v = __builtin_bit_cast(v4u, mfma_dequant(P[j], d));
+            const v4u v = __builtin_bit_cast(v4u, mfma_dequant(P[j], d, kx));
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const int k = kb * kGroup + 32 * j + 16 * (e >> 2) + 4 * (l >> 4) + (e & 3);
+                const int k = kb * kGroup + 32 * j + 8 * (l >> 4) + e;
                 w[n * K + k] = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
             }
         }
@@ -253,6 +274,7 @@ __global__ void k_dequant_valu(const uint4 *__restrict__ codes, const void *__re
     const size_t nblocks = (size_t)(N / kTileN) * Kb;
     const int l = threadIdx.x & 63;
     const int b2 = (l >> 2) & 3;
+    const ExtractConsts kx;
     for (size_t b = (size_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); b < nblocks;
          b += (size_t)gridDim.x * (blockDim.x >> 6)) {
         const uint4 c = codes[b * 64 + l];
@@ -260,15 +282,15 @@ __global__ void k_dequant_valu(const uint4 *__restrict__ codes, const void *__re
         for (int r = 0; r < 4; ++r) s4[r] = load_sz<SYM>(sz, b * kTileN + 4 * b2 + r);
         const ValuDeq d = valu_setup(s4);
         const uint32_t P[4] = {c.x, c.y, c.z, c.w};
-        const int t = (int)(b / Kb), kb = (int)(b % Kb);
+        const int kb = (int)(b / (N / kTileN)), t = (int)(b % (N / kTileN));
         for (int j = 0; j < 4; ++j) {
             uint32_t pr[4];
-            valu_dequant(P[j], d, pr);
+            valu_dequant(P[j], d, kx, pr);
             for (int r = 0; r < 4; ++r) {
                 const size_t n = (size_t)t * kTileN + 4 * b2 + r;
-                const int k0 = kb * kGroup + 32 * j + 4 * (l >> 4) + (l & 3);
+                const int k0 = kb * kGroup + 32 * j + 8 * (l >> 4) + (l & 3);
                 w[n * K + k0] = (uint16_t)(pr[r] & 0xFFFFu);
-                w[n * K + k0 + 16] = (uint16_t)(pr[r] >> 16);
+                w[n * K + k0 + 4] = (uint16_t)(pr[r] >> 16);
             }
         }
     }
@@ -280,47 +302,52 @@ __global__ void k_dequant_valu(const uint4 *__restrict__ codes, const void *__re
 struct WgWork { int c, jn, t0, Tn, g0, Kc; };
 __device__ inline WgWork wg_work(const FwdArgs &a, int bid) {
     WgWork w;
-    w.c = bid / a.Gn;
+    w.c = bid / a.Gn;                         // once per workgroup, scalar
     w.jn = bid - w.c * a.Gn;
-    w.t0 = (int)(((long long)w.jn * a.Nt) / a.Gn);
-    w.Tn = (int)(((long long)(w.jn + 1) * a.Nt) / a.Gn) - w.t0;
-    w.g0 = (int)(((long long)w.c * a.Kb) / a.S);
-    w.Kc = (int)(((long long)(w.c + 1) * a.Kb) / a.S) - w.g0;
+    w.t0 = w.jn * a.Nq + min(w.jn, a.Nr);
+    w.Tn = a.Nq + (w.jn < a.Nr ? 1 : 0);
+    w.g0 = w.c * a.Kq + min(w.c, a.Kr);
+    w.Kc = a.Kq + (w.c < a.Kr ? 1 : 0);
     return w;
 }
 
-// Writes the workgroup's accumulated tiles: straight to y as bf16 when the
-// whole K range was covered (S == 1); otherwise as fp32 partial sums, and
-// the last of the S workgroups of this column range adds the S partials in
-// chunk order (a fixed order, so results do not depend on arrival order),
-// rounds once and writes y.
-__device__ inline void write_out(const FwdArgs &a, const WgWork &w, const float *accs, int rows) {
-    const int tid = threadIdx.x;
-    const int items = w.Tn * a.M * 2;              // half rows of 8 columns
-    const bool direct = (a.S == 1);
-    for (int it = tid; it < items; it += blockDim.x) {
-        const int tl = it / (a.M * 2);
-        const int rem = it - tl * a.M * 2;
-        const int m = rem >> 1, hh = rem & 1;
-        const float *src = accs + ((size_t)tl * rows + m) * kAccPad + 8 * hh;
-        const size_t n = (size_t)(w.t0 + tl) * kTileN + 8 * hh;
-        if (direct) {
-            uint4 o;
-            o.x = cvt_pk_bf16(src[0], src[1]);
-            o.y = cvt_pk_bf16(src[2], src[3]);
-            o.z = cvt_pk_bf16(src[4], src[5]);
-            o.w = cvt_pk_bf16(src[6], src[7]);
-            *(uint4 *)(a.y + (size_t)m * a.N + n) = o;
-        } else {
-            float4 *dst = (float4 *)(a.ws + ((size_t)w.c * a.M + m) * a.N + n);
-            dst[0] = make_float4(src[0], src[1], src[2], src[3]);
-            dst[1] = make_float4(src[4], src[5], src[6], src[7]);
-        }
-    }
-    if (direct) return;
+// Range [u0, u1) of the U = Tn * Kc blocks (tile-major) that wave i of a
+// workgroup handles: U / kWaves blocks each, one more for the first U % kWaves.
+__device__ inline void wave_range(int U, int i, int &u0, int &u1) {
+    const int q = U / kWaves, r = U % kWaves;    // kWaves is a power of two
+    u0 = i * q + min(i, r);
+    u1 = u0 + q + (i < r ? 1 : 0);
+}
 
+// Walks the blocks of a wave's range in tile-major order u = tl * Kc + kbl:
+// block index (g0 + kbl) * Nt + t0 + tl and position (tile tl, group kbl)
+// within the workgroup's work, no division.
+struct BlockWalk {
+    int tl, kbl;
+    size_t b;
+    __device__ inline void start(const WgWork &w, int Nt, int u) {
+        tl = 0;
+        kbl = u;
+        while (kbl >= w.Kc) { kbl -= w.Kc; ++tl; }   // u < Tn * Kc: at most Tn steps, once
+        b = (size_t)(w.g0 + kbl) * Nt + w.t0 + tl;
+    }
+    __device__ inline void next(const WgWork &w, int Nt) {
+        if (++kbl == w.Kc) { kbl = 0; ++tl; b -= (size_t)(w.Kc - 1) * Nt - 1; }
+        else b += Nt;
+    }
+};
+
+// The last of the S workgroups of a column range adds the S fp32 partials in
+// chunk order (fixed order) and writes y.
+__device__ inline void reduce_chunks(const FwdArgs &a, const WgWork &w) {
+    const int tid = threadIdx.x;
+    const int items = w.Tn * a.M * 2;
+    // Publish: the barrier completes every wave's partial-sum stores (to L2);
+    // one agent-scope acq_rel atomic then writes the L2 back before counting
+    // this arrival and, for the last arrival, invalidates the caches so the
+    // other workgroups' partials are read fresh.  One fence per workgroup,
+    // not one per thread.
     __shared__ int s_last;
-    __threadfence();
     __syncthreads();
     if (tid == 0) {
         const uint32_t old = __hip_atomic_fetch_add(&a.counters[w.jn], 1u, __ATOMIC_ACQ_REL,
@@ -329,7 +356,6 @@ __device__ inline void write_out(const FwdArgs &a, const WgWork &w, const float 
     }
     __syncthreads();
     if (!s_last) return;
-    __threadfence();
     for (int it = tid; it < items; it += blockDim.x) {
         const int tl = it / (a.M * 2);
         const int rem = it - tl * a.M * 2;
@@ -352,97 +378,186 @@ __device__ inline void write_out(const FwdArgs &a, const WgWork &w, const float 
     if (tid == 0) __hip_atomic_store(&a.counters[w.jn], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-constexpr int kDepth = 4;   // 1 KiB blocks in flight per wave
+// Writes the workgroup's results.  Each wave left one partial sum per column
+// tile it touched in LDS slot (wave + tile); the tile's sum adds those slots in
+// wave order.  With the whole K range covered (S == 1) the sum goes to y as
+// bf16; otherwise it goes to the fp32 workspace, and the last of the S
+// workgroups of this column range adds the S partials in chunk order and
+// writes y.  Every sum runs in a fixed order, so results do not depend on
+// timing: repeated calls give identical bits.
+__device__ inline void write_out(const FwdArgs &a, const WgWork &w, const float *slots, int rows) {
+    const int tid = threadIdx.x;
+    const int items = w.Tn * a.M * 2;              // half rows of 8 columns
+    const int U = w.Tn * w.Kc;
+    const bool direct = (a.S == 1);
+    for (int it = tid; it < items; it += blockDim.x) {
+        const int tl = it / (a.M * 2);
+        const int rem = it - tl * a.M * 2;
+        const int m = rem >> 1, hh = rem & 1;
+        float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int i = 0; i < kWaves; ++i) {
+            int u0, u1;
+            wave_range(U, i, u0, u1);
+            if (u0 < u1 && u0 < (tl + 1) * w.Kc && u1 > tl * w.Kc) {
+                const float4 *src = (const float4 *)(slots + ((size_t)(i + tl) * rows + m) * 16 + 8 * hh);
+                const float4 v0 = src[0], v1 = src[1];
+                s[0] += v0.x; s[1] += v0.y; s[2] += v0.z; s[3] += v0.w;
+                s[4] += v1.x; s[5] += v1.y; s[6] += v1.z; s[7] += v1.w;
+            }
+        }
+        const size_t n = (size_t)(w.t0 + tl) * kTileN + 8 * hh;
+        if (direct) {
+            uint4 o;
+            o.x = cvt_pk_bf16(s[0], s[1]);
+            o.y = cvt_pk_bf16(s[2], s[3]);
+            o.z = cvt_pk_bf16(s[4], s[5]);
+            o.w = cvt_pk_bf16(s[6], s[7]);
+            *(uint4 *)(a.y + (size_t)m * a.N + n) = o;
+        } else {
+            float4 *dst = (float4 *)(a.ws + ((size_t)w.c * a.M + m) * a.N + n);
+            dst[0] = make_float4(s[0], s[1], s[2], s[3]);
+            dst[1] = make_float4(s[4], s[5], s[6], s[7]);
+        }
+    }
+    if (!direct) reduce_chunks(a, w);
+}
+
+constexpr int kStageMax = (kXChunksMax + kThreads - 1) / kThreads;
+
+// Barrier for LDS hand-off only.  __syncthreads() also waits for every
+// outstanding global load, which would drain the weight prefetch.
+__device__ inline void lds_barrier() {
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// x chunks staged per thread: the planner never gives a workgroup more than
+// kXChunksMax 16-byte chunks, so one unrolled batch per thread covers them.
+// The chunk sequence idx = bb * kThreads + tid is walked as (row m, chunk q8)
+// with increments only.
+struct StageWalk {
+    int m, q8, dm, dq;
+    __device__ inline void start(int n8, int tid) {
+        dm = kThreads / n8;
+        dq = kThreads - dm * n8;
+        m = tid / n8;                 // once per thread
+        q8 = tid - m * n8;
+    }
+    __device__ inline void next(int n8) {
+        m += dm;
+        q8 += dq;
+        if (q8 >= n8) { q8 -= n8; ++m; }
+    }
+};
 
 // ---- SKINNY: matrix-core dequantization + v_mfma_f32_16x16x32_bf16 --------
 //
 // A workgroup owns K chunk c (groups [g0, g0 + Kc)) of column tiles
 // [t0, t0 + Tn).  It stages x[:, chunk] in LDS once, in MFMA B-operand order,
-// then its 8 waves split the Tn * Kc blocks evenly (tile-major order), each
-// streaming its blocks with kDepth 128-bit loads in flight.  A wave adds its
-// tile sums into LDS accumulators when it leaves a tile; the workgroup then
-// writes y (or partials).
+// while its first weight blocks are already in flight; its waves then split
+// the Tn * Kc blocks evenly (tile-major order), each keeping kDepth 1 KiB
+// blocks in flight.  A wave leaves one partial sum per tile it touches in an
+// LDS slot; write_out() adds them in a fixed order.
 //
-// x in LDS: 16-byte fragments F[kbl][g][j][row], row < 16 * MT; fragment
-// (kbl, g, j, row) = x[row][k] for k = 128(g0 + kbl) + 32j + 16h + 4g + i,
-// element 4h + i.  Lane l of m-tile mt reads fragment (kbl, l >> 4, j, 16 mt + (l & 15)).
+// x in LDS: 16-byte fragments, fragment (kbl, c, row) = x[row][k0 .. k0 + 8)
+// with k0 = 128(g0 + kbl) + 8c, c = 4j + g < 16, stored at slot
+// (16 kbl + c) * MR + (row & ~15) + ((row & 15) ^ c).  The XOR swizzle keeps
+// both the staging writes (16 lanes = 16 consecutive c of one row) and the
+// operand reads (16 lanes = 16 rows of one c) on distinct LDS banks.  Lane l
+// of m-tile mt reads c = 4j + (l >> 4), row 16 mt + (l & 15).
 template <int MT, bool SYM>
 __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     constexpr int MR = 16 * MT;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: keeps the walk on the scalar unit
+    const ExtractConsts kx;
     const WgWork w = wg_work(a, blockIdx.x);
     uint4 *xs = (uint4 *)smem;
-    float *accs = (float *)(smem + (size_t)w.Kc * MR * 256);
-
-    // stage x chunk (rows >= M are zero)
-    {
-        const int n8 = w.Kc * 16;
-        for (int idx = tid; idx < MR * n8; idx += kThreads) {
-            const int m = idx / n8, q8 = idx - m * n8;
-            const int kbl = q8 >> 4, r8 = q8 & 15;
-            uint4 v = make_uint4(0, 0, 0, 0);
-            if (m < a.M) v = *(const uint4 *)(a.x + (size_t)m * a.K + (size_t)(w.g0 + kbl) * kGroup + r8 * 8);
-            const int j = r8 >> 2, p0 = (r8 & 3) * 2;
-            uint2 *d0 = (uint2 *)&xs[((kbl * 4 + (p0 & 3)) * 4 + j) * MR + m] + (p0 >> 2);
-            uint2 *d1 = (uint2 *)&xs[((kbl * 4 + ((p0 + 1) & 3)) * 4 + j) * MR + m] + ((p0 + 1) >> 2);
-            *d0 = make_uint2(v.x, v.y);
-            *d1 = make_uint2(v.z, v.w);
-        }
-        for (int idx = tid; idx < w.Tn * MR * kAccPad; idx += kThreads) accs[idx] = 0.0f;
-    }
-    __syncthreads();
+    float *slots = (float *)(smem + (size_t)w.Kc * MR * 256);
 
     const int U = w.Tn * w.Kc;
-    const int u0 = (int)(((long long)wave * U) / kWaves);
-    const int u1 = (int)(((long long)(wave + 1) * U) / kWaves);
+    int u0, u1;
+    wave_range(U, wave, u0, u1);
     const int lm = lane & 15, lg = lane >> 4;
     const uint32_t shift = (lane & 1) * 16, keep_lo = (lane & 2) ? 0u : 0xFFFFFFFFu;
 
-    if (u0 < u1) {
-        auto block_of = [&](int u) -> size_t {
-            const int tl = u / w.Kc;
-            return (size_t)(w.t0 + tl) * a.Kb + w.g0 + (u - tl * w.Kc);
-        };
-        uint4 cb[kDepth];
-        uint32_t sb[kDepth];
+    // 1) issue the x loads of the whole chunk (rows >= M read as zero)
+    const int n8 = w.Kc * 16;
+    const int total = MR * n8;
+    uint4 v[kStageMax];
+    {
+        StageWalk sw;
+        sw.start(n8, tid);
 #pragma unroll
-        for (int d = 0; d < kDepth; ++d) {
-            const size_t b = block_of(min(u0 + d, u1 - 1));
-            cb[d] = a.codes[b * 64 + lane];
-            sb[d] = load_sz<SYM>(a.sz, b * kTileN + lm);
+        for (int bb = 0; bb < kStageMax; ++bb) {
+            v[bb] = make_uint4(0, 0, 0, 0);
+            if (bb * kThreads + tid < total && sw.m < a.M)
+                v[bb] = *(const uint4 *)(a.x + (size_t)sw.m * a.K + (size_t)(w.g0 + (sw.q8 >> 4)) * kGroup +
+                                         (sw.q8 & 15) * 8);
+            sw.next(n8);
         }
+    }
+    // 2) then the first weight blocks (younger than the x loads, so waiting
+    //    for x below does not wait for them).  A wave with an empty range
+    //    re-reads one block, which is harmless.
+    BlockWalk pw;                       // prefetch position
+    pw.start(w, a.Nt, min(u0, U - 1));
+    int up = u0;                        // block index pw points at
+    uint4 cb[kDepth];
+    uint32_t sb[kDepth];
+#pragma unroll
+    for (int d = 0; d < kDepth; ++d) {
+        cb[d] = load_block(a.codes, pw.b * 64 + lane);
+        sb[d] = load_sz<SYM>(a.sz, pw.b * kTileN + lm);
+        if (up + 1 < u1) { pw.next(w, a.Nt); ++up; }
+    }
+    // 3) write x to LDS in fragment order
+    {
+        StageWalk sw;
+        sw.start(n8, tid);
+#pragma unroll
+        for (int bb = 0; bb < kStageMax; ++bb) {
+            if (bb * kThreads + tid < total) {
+                const int c = sw.q8 & 15;          // (kbl, c) with kbl = q8 >> 4
+                xs[sw.q8 * MR + (sw.m & ~15) + ((sw.m & 15) ^ c)] = v[bb];
+            }
+            sw.next(n8);
+        }
+    }
+    lds_barrier();
+
+    if (u0 < u1) {
         v4f acc[MT];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[mt] = v4f{0, 0, 0, 0};
+        BlockWalk cw;                   // consume position
+        cw.start(w, a.Nt, u0);
 
-        auto consume = [&](int u, const uint4 &cw, uint32_t szw) {
-            const int tl = u / w.Kc, kbl = u - tl * w.Kc;
+        auto consume = [&](int u, const uint4 &cq, uint32_t szw) {
             v8bf xf[MT][4];
 #pragma unroll
             for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
-                    xf[mt][j] = __builtin_bit_cast(v8bf, xs[((kbl * 4 + lg) * 4 + j) * MR + 16 * mt + lm]);
+                    xf[mt][j] = __builtin_bit_cast(v8bf, xs[(cw.kbl * 16 + 4 * j + lg) * MR + 16 * mt + (lm ^ (4 * j + lg))]);
             const MfmaDeq d = mfma_setup(szw, shift, keep_lo);
-            const uint32_t P[4] = {cw.x, cw.y, cw.z, cw.w};
+            const uint32_t P[4] = {cq.x, cq.y, cq.z, cq.w};
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                const v8bf wa = mfma_dequant(P[j], d);
+                const v8bf wa = mfma_dequant(P[j], d, kx);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
                     acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, xf[mt][j], acc[mt], 0, 0, 0);
             }
-            if (kbl == w.Kc - 1 || u == u1 - 1) {
+            if (cw.kbl == w.Kc - 1 || u == u1 - 1) {
                 // D of the 16x16 op: lane l holds rows n = 4(l >> 4) + v of column m = l & 15
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
-#pragma unroll
-                    for (int v = 0; v < 4; ++v)
-                        atomicAdd(&accs[((size_t)tl * MR + 16 * mt + lm) * kAccPad + 4 * lg + v], acc[mt][v]);
+                    *(v4f *)(slots + ((size_t)(wave + cw.tl) * MR + 16 * mt + lm) * 16 + 4 * lg) = acc[mt];
                     acc[mt] = v4f{0, 0, 0, 0};
                 }
             }
+            cw.next(w, a.Nt);
         };
 
         int u = u0;
@@ -450,142 +565,283 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
 #pragma unroll
             for (int d = 0; d < kDepth; ++d) {
                 consume(u + d, cb[d], sb[d]);
-                const size_t b = block_of(min(u + d + kDepth, u1 - 1));
-                cb[d] = a.codes[b * 64 + lane];
-                sb[d] = load_sz<SYM>(a.sz, b * kTileN + lm);
+                cb[d] = load_block(a.codes, pw.b * 64 + lane);
+                sb[d] = load_sz<SYM>(a.sz, pw.b * kTileN + lm);
+                if (up + 1 < u1) { pw.next(w, a.Nt); ++up; }
             }
         }
 #pragma unroll
         for (int d = 0; d < kDepth; ++d)
             if (u + d < u1) consume(u + d, cb[d], sb[d]);
     }
-    __syncthreads();
-    write_out(a, w, accs, MR);
+    lds_barrier();
+    write_out(a, w, slots, MR);
 }
 
-// ---- GEMV: vector-ALU dequantization + v_dot2_f32_bf16 --------------------
+// ---- register-resident kernels (M <= 16) -------------------------------
 //
-// Same work split as SKINNY.  x in LDS: for row m, group kbl and
-// kk = 4g + i (g = l >> 4, i = l & 3), 16 bytes holding the bf16 pairs
-// (x[m][k], x[m][k + 16]) with k = 128(g0 + kbl) + 32j + kk for j = 0..3.
-template <int MV, bool SYM>
-__global__ void __launch_bounds__(kThreads) k_gemv(FwdArgs a) {
-    extern __shared__ __align__(16) unsigned char smem[];
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const WgWork w = wg_work(a, blockIdx.x);
-    uint4 *xg = (uint4 *)smem;
-    float *accs = (float *)(smem + (size_t)w.Kc * MV * 256);
+// A workgroup owns K chunk c (groups [g0, g0 + Kc)) of column tiles
+// [t0, t0 + Tn), Tn <= kTnMax.  Its waves split the Tn * Kc blocks evenly in
+// group-major order u = kbl * Tn + tl, so a wave covers only ~Kc / kWaves + 2
+// groups and loads the x it needs straight into registers: no x staging in
+// LDS and no barrier before the main loop.  Per group a wave loads every one
+// of its tiles' blocks (contiguous KiB in the device layout) plus that
+// group's x, one group ahead of the compute (two register sets, A and B).
+// Each wave keeps one accumulator per tile; at the end it writes them to its
+// LDS slots and write_out_waves() adds the waves' slots in wave order.
+//
+// Out-of-range tiles of a wave's first and last group still load (a valid
+// block of the group) so that the loads stay unconditional and the compiler
+// can count them; they are not computed.
 
-    {
-        uint16_t *xh = (uint16_t *)smem;
-        const int n8 = w.Kc * 16;
-        for (int idx = tid; idx < MV * n8; idx += kThreads) {
-            const int m = idx / n8, q8 = idx - m * n8;
-            const int kbl = q8 >> 4, r8 = q8 & 15;
-            const uint4 v = *(const uint4 *)(a.x + (size_t)m * a.K + (size_t)(w.g0 + kbl) * kGroup + r8 * 8);
-            const uint32_t vv[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int kg = r8 * 8 + e;                 // k within the group
-                const int j = kg >> 5, k32 = kg & 31;
-                const int hh = k32 >> 4, kk = k32 & 15;
-                xh[((((size_t)m * w.Kc + kbl) * 16 + kk) * 4 + j) * 2 + hh] =
-                    (uint16_t)(vv[e >> 1] >> (16 * (e & 1)));
-            }
+// Sum over the waves' slots (fixed order) and write y, or fp32 partials plus
+// the last-arrival reduction when the K range is cut (S > 1).  Slot (wave, tl)
+// holds rows x 16 fp32 (row-major, 16 columns).
+__device__ inline void write_out_waves(const FwdArgs &a, const WgWork &w, const float *slots, int rows) {
+    const int tid = threadIdx.x;
+    const int items = w.Tn * a.M * 2;              // half rows of 8 columns
+    const bool direct = (a.S == 1);
+    for (int it = tid; it < items; it += blockDim.x) {
+        const int tl = it / (a.M * 2);
+        const int rem = it - tl * a.M * 2;
+        const int m = rem >> 1, hh = rem & 1;
+        float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        for (int i = 0; i < kWaves; ++i) {
+            const float4 *src = (const float4 *)(slots + (((size_t)i * kTnMax + tl) * rows + m) * 16 + 8 * hh);
+            const float4 v0 = src[0], v1 = src[1];
+            s[0] += v0.x; s[1] += v0.y; s[2] += v0.z; s[3] += v0.w;
+            s[4] += v1.x; s[5] += v1.y; s[6] += v1.z; s[7] += v1.w;
         }
-        for (int idx = tid; idx < w.Tn * MV * kAccPad; idx += kThreads) accs[idx] = 0.0f;
+        const size_t n = (size_t)(w.t0 + tl) * kTileN + 8 * hh;
+        if (direct) {
+            uint4 o;
+            o.x = cvt_pk_bf16(s[0], s[1]);
+            o.y = cvt_pk_bf16(s[2], s[3]);
+            o.z = cvt_pk_bf16(s[4], s[5]);
+            o.w = cvt_pk_bf16(s[6], s[7]);
+            *(uint4 *)(a.y + (size_t)m * a.N + n) = o;
+        } else {
+            float4 *dst = (float4 *)(a.ws + ((size_t)w.c * a.M + m) * a.N + n);
+            dst[0] = make_float4(s[0], s[1], s[2], s[3]);
+            dst[1] = make_float4(s[4], s[5], s[6], s[7]);
+        }
     }
-    __syncthreads();
+    if (!direct) reduce_chunks(a, w);
+}
 
-    const int U = w.Tn * w.Kc;
-    const int u0 = (int)(((long long)wave * U) / kWaves);
-    const int u1 = (int)(((long long)(wave + 1) * U) / kWaves);
-    const int b2 = (lane >> 2) & 3;
-    const int kk = 4 * (lane >> 4) + (lane & 3);
+// The wave's groups [kg0, kg1] and, in the first and last of them, the tile
+// range [ta0, Tn) and [0, tb1).
+struct WaveGroups {
+    int kg0, kg1, ta0, tb1;
+    __device__ inline void init(int u0, int u1, int Tn) {
+        kg0 = u0 / Tn;                // scalar, once per wave
+        kg1 = (u1 - 1) / Tn;
+        ta0 = u0 - kg0 * Tn;
+        tb1 = u1 - kg1 * Tn;
+    }
+    __device__ inline int ta(int kbl) const { return kbl == kg0 ? ta0 : 0; }
+    __device__ inline int tb(int kbl, int Tn) const { return kbl == kg1 ? tb1 : Tn; }
+};
+
+template <bool SYM>
+struct MfmaGroup {
+    uint4 c[kTnMax];
+    uint32_t s[kTnMax];
+    v8bf x[4];
+};
+
+// x fragment of lane l for step j of group kb: row l & 15, k = 128 kb + 32 j + 8 (l >> 4).
+// Lanes of rows >= M read row M - 1: in the 16x16 product those lanes only
+// feed output columns >= M, which are never written.
+__device__ inline v8bf load_xfrag(const FwdArgs &a, int kb, int j, int lane) {
+    const int m = min(lane & 15, a.M - 1);
+    return __builtin_bit_cast(v8bf, *(const uint4 *)(a.x + (size_t)m * a.K + (size_t)kb * kGroup + 32 * j +
+                                                      8 * (lane >> 4)));
+}
+
+template <bool SYM>
+__global__ void __launch_bounds__(kThreads) k_mfma16(FwdArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    float *slots = (float *)smem;                  // [kWaves][kTnMax][16][16]
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const ExtractConsts kx;
+    const WgWork w = wg_work(a, blockIdx.x);
+    const int Tn = w.Tn;
+    int u0, u1;
+    wave_range(Tn * w.Kc, wave, u0, u1);
+    const int lm = lane & 15, lg = lane >> 4;
+    const uint32_t shift = (lane & 1) * 16, keep_lo = (lane & 2) ? 0u : 0xFFFFFFFFu;
+
+    v4f acc[kTnMax];
+#pragma unroll
+    for (int t = 0; t < kTnMax; ++t) acc[t] = v4f{0, 0, 0, 0};
 
     if (u0 < u1) {
-        auto block_of = [&](int u) -> size_t {
-            const int tl = u / w.Kc;
-            return (size_t)(w.t0 + tl) * a.Kb + w.g0 + (u - tl * w.Kc);
+        WaveGroups wg;
+        wg.init(u0, u1, Tn);
+        auto load_group = [&](MfmaGroup<SYM> &B, int kbl) {
+            const int ta = wg.ta(kbl), tb = wg.tb(kbl, Tn);
+            const size_t base = (size_t)(w.g0 + kbl) * a.Nt + w.t0;
+#pragma unroll
+            for (int t = 0; t < kTnMax; ++t) {
+                const size_t b = base + min(max(t, ta), tb - 1);
+                B.c[t] = load_block(a.codes, b * 64 + lane);
+                B.s[t] = load_sz<SYM>(a.sz, b * kTileN + lm);
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) B.x[j] = load_xfrag(a, w.g0 + kbl, j, lane);
         };
-        auto load_sz4 = [&](size_t b, uint32_t s4[4]) {
-            if constexpr (SYM) {
-                const uint2 h = *(const uint2 *)((const uint16_t *)a.sz + b * kTileN + 4 * b2);
-                s4[0] = (h.x & 0xFFFFu) | (0x4100u << 16);
-                s4[1] = (h.x >> 16) | (0x4100u << 16);
-                s4[2] = (h.y & 0xFFFFu) | (0x4100u << 16);
-                s4[3] = (h.y >> 16) | (0x4100u << 16);
-            } else {
-                const uint4 q = *(const uint4 *)((const uint32_t *)a.sz + b * kTileN + 4 * b2);
-                s4[0] = q.x; s4[1] = q.y; s4[2] = q.z; s4[3] = q.w;
+        auto compute_group = [&](const MfmaGroup<SYM> &B, int kbl) {
+            const int ta = wg.ta(kbl), tb = wg.tb(kbl, Tn);
+#pragma unroll
+            for (int t = 0; t < kTnMax; ++t) {
+                if (t >= ta && t < tb) {
+                    const MfmaDeq d = mfma_setup(B.s[t], shift, keep_lo);
+                    const uint32_t P[4] = {B.c[t].x, B.c[t].y, B.c[t].z, B.c[t].w};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j)
+                        acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(mfma_dequant(P[j], d, kx), B.x[j], acc[t], 0,
+                                                                         0, 0);
+                }
             }
         };
-        uint4 cb[kDepth];
-        uint32_t sb[kDepth][4];
-#pragma unroll
-        for (int d = 0; d < kDepth; ++d) {
-            const size_t b = block_of(min(u0 + d, u1 - 1));
-            cb[d] = a.codes[b * 64 + lane];
-            load_sz4(b, sb[d]);
+        // The next group's loads are issued unconditionally (the last group
+        // is re-read at the end, from cache): a conditional load would
+        // leave the compiler unsure how many loads are younger than the ones
+        // it waits for, and it would then drain every load in flight.
+        MfmaGroup<SYM> A, B;
+        load_group(A, wg.kg0);
+        for (int kbl = wg.kg0; kbl <= wg.kg1; kbl += 2) {
+            load_group(B, min(kbl + 1, wg.kg1));
+            compute_group(A, kbl);
+            load_group(A, min(kbl + 2, wg.kg1));
+            if (kbl + 1 <= wg.kg1) compute_group(B, kbl + 1);
         }
-        float acc[MV][4];
+    }
+    // D of the 16x16 op: lane l holds rows n = 4(l >> 4) + v of column m = l & 15
+#pragma unroll
+    for (int t = 0; t < kTnMax; ++t)
+        if (t < Tn) *(v4f *)(slots + (((size_t)wave * kTnMax + t) * 16 + lm) * 16 + 4 * lg) = acc[t];
+    lds_barrier();
+    write_out_waves(a, w, slots, 16);
+}
+
+// ---- GEMV: vector-ALU dequantization + v_dot2_f32_bf16 (M <= 4) ---------
+//
+// Same walk as k_mfma16.  Lane l (b2 = (l >> 2) & 3, g = l >> 4, i = l & 3)
+// holds, for every row m and step j, the bf16 pair (x[m][k], x[m][k + 4]) with
+// k = 128 kb + 32 j + 8 g + i, matching valu_dequant()'s weight pairs.
+template <int MV, bool SYM>
+struct GemvGroup {
+    uint4 c[kTnMaxGemv];
+    uint4 s[kTnMaxGemv];
+    uint32_t x[MV][4];
+};
+
+template <int MV, bool SYM>
+__global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    float *slots = (float *)smem;                  // [kWaves][kTnMax][MV][16]
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const ExtractConsts kx;
+    const WgWork w = wg_work(a, blockIdx.x);
+    const int Tn = w.Tn;
+    int u0, u1;
+    wave_range(Tn * w.Kc, wave, u0, u1);
+    const int b2 = (lane >> 2) & 3, li = lane & 3, lg = lane >> 4;
+    const uint32_t xsel = (li & 1) ? 0x07060302u : 0x05040100u;   // high or low halves
+
+    float acc[kTnMaxGemv][MV][4];
+#pragma unroll
+    for (int t = 0; t < kTnMaxGemv; ++t)
 #pragma unroll
         for (int m = 0; m < MV; ++m)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) acc[m][r] = 0.0f;
+            for (int r = 0; r < 4; ++r) acc[t][m][r] = 0.0f;
 
-        auto consume = [&](int u, const uint4 &cw, const uint32_t s4[4]) {
-            const int tl = u / w.Kc, kbl = u - tl * w.Kc;
-            uint4 xv[MV];
+    if (u0 < u1) {
+        WaveGroups wg;
+        wg.init(u0, u1, Tn);
+        auto load_group = [&](GemvGroup<MV, SYM> &B, int kbl) {
+            const int ta = wg.ta(kbl), tb = wg.tb(kbl, Tn);
+            const size_t base = (size_t)(w.g0 + kbl) * a.Nt + w.t0;
 #pragma unroll
-            for (int m = 0; m < MV; ++m) xv[m] = xg[((size_t)m * w.Kc + kbl) * 16 + kk];
-            const ValuDeq d = valu_setup(s4);
-            const uint32_t P[4] = {cw.x, cw.y, cw.z, cw.w};
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                uint32_t pr[4];
-                valu_dequant(P[j], d, pr);
-#pragma unroll
-                for (int m = 0; m < MV; ++m) {
-                    const uint32_t xp = (j == 0) ? xv[m].x : (j == 1) ? xv[m].y : (j == 2) ? xv[m].z : xv[m].w;
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) acc[m][r] = dot2(pr[r], xp, acc[m][r]);
+            for (int t = 0; t < kTnMaxGemv; ++t) {
+                const size_t b = base + min(max(t, ta), tb - 1);
+                B.c[t] = load_block(a.codes, b * 64 + lane);
+                if constexpr (SYM) {
+                    const uint2 h = *(const uint2 *)((const uint16_t *)a.sz + b * kTileN + 4 * b2);
+                    B.s[t] = make_uint4((h.x & 0xFFFFu) | (0x4100u << 16), (h.x >> 16) | (0x4100u << 16),
+                                        (h.y & 0xFFFFu) | (0x4100u << 16), (h.y >> 16) | (0x4100u << 16));
+                } else {
+                    B.s[t] = *(const uint4 *)((const uint32_t *)a.sz + b * kTileN + 4 * b2);
                 }
             }
-            if (kbl == w.Kc - 1 || u == u1 - 1) {
-                // sum over the 16 lanes sharing b2 (lane bits 0, 1, 4, 5)
 #pragma unroll
-                for (int m = 0; m < MV; ++m)
+            for (int m = 0; m < MV; ++m)
 #pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        float v = acc[m][r];
-                        v += __shfl_xor(v, 1);
-                        v += __shfl_xor(v, 2);
-                        v += __shfl_xor(v, 16);
-                        v += __shfl_xor(v, 32);
-                        if ((lane & 0x33) == 0)
-                            atomicAdd(&accs[((size_t)tl * MV + m) * kAccPad + 4 * b2 + r], v);
-                        acc[m][r] = 0.0f;
+                for (int j = 0; j < 4; ++j) {
+                    const uint4 q = *(const uint4 *)(a.x + (size_t)m * a.K + (size_t)(w.g0 + kbl) * kGroup + 32 * j +
+                                                     8 * lg);
+                    const uint32_t lo = (li < 2) ? q.x : q.y, hi = (li < 2) ? q.z : q.w;
+                    B.x[m][j] = __builtin_amdgcn_perm(hi, lo, xsel);
+                }
+        };
+        auto compute_group = [&](const GemvGroup<MV, SYM> &B, int kbl) {
+            const int ta = wg.ta(kbl), tb = wg.tb(kbl, Tn);
+#pragma unroll
+            for (int t = 0; t < kTnMaxGemv; ++t) {
+                if (t >= ta && t < tb) {
+                    const uint32_t s4[4] = {B.s[t].x, B.s[t].y, B.s[t].z, B.s[t].w};
+                    const ValuDeq d = valu_setup(s4);
+                    const uint32_t P[4] = {B.c[t].x, B.c[t].y, B.c[t].z, B.c[t].w};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        uint32_t pr[4];
+                        valu_dequant(P[j], d, kx, pr);
+#pragma unroll
+                        for (int m = 0; m < MV; ++m)
+#pragma unroll
+                            for (int r = 0; r < 4; ++r) acc[t][m][r] = dot2(pr[r], B.x[m][j], acc[t][m][r]);
                     }
+                }
             }
         };
-
-        int u = u0;
-        for (; u + kDepth <= u1; u += kDepth) {
+        GemvGroup<MV, SYM> A, B;          // unconditional next-group loads, see k_mfma16
+        load_group(A, wg.kg0);
+        for (int kbl = wg.kg0; kbl <= wg.kg1; kbl += 2) {
+            load_group(B, min(kbl + 1, wg.kg1));
+            compute_group(A, kbl);
+            load_group(A, min(kbl + 2, wg.kg1));
+            if (kbl + 1 <= wg.kg1) compute_group(B, kbl + 1);
+        }
+    }
+    // sum over the 16 lanes sharing b2 (lane bits 0, 1, 4, 5), then one lane per b2 writes
 #pragma unroll
-            for (int d = 0; d < kDepth; ++d) {
-                consume(u + d, cb[d], sb[d]);
-                const size_t b = block_of(min(u + d + kDepth, u1 - 1));
-                cb[d] = a.codes[b * 64 + lane];
-                load_sz4(b, sb[d]);
+    for (int t = 0; t < kTnMaxGemv; ++t) {
+        if (t < Tn) {
+#pragma unroll
+            for (int m = 0; m < MV; ++m) {
+                float t4[4];
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    float v = acc[t][m][r];
+                    v += __shfl_xor(v, 1);
+                    v += __shfl_xor(v, 2);
+                    v += __shfl_xor(v, 16);
+                    v += __shfl_xor(v, 32);
+                    t4[r] = v;
+                }
+                if ((lane & 0x33) == 0)
+                    *(float4 *)(slots + (((size_t)wave * kTnMax + t) * MV + m) * 16 + 4 * b2) =
+                        make_float4(t4[0], t4[1], t4[2], t4[3]);
             }
         }
-#pragma unroll
-        for (int d = 0; d < kDepth; ++d)
-            if (u + d < u1) consume(u + d, cb[d], sb[d]);
     }
-    __syncthreads();
-    write_out(a, w, accs, MV);
+    lds_barrier();
+    write_out_waves(a, w, slots, MV);
 }
 
 // ------------------------------------------------------------------ host launchers
@@ -631,64 +887,59 @@ hipError_t launch_dequant(int routine, const uint4 *codes, const void *sz, bool 
 typedef void (*FwdKernel)(FwdArgs);
 
 template <bool SYM>
-static FwdKernel pick(int path, int mrows) {
-    if (path == kSkinny) {
-        switch (mrows) {
-            case 16: return k_skinny<1, SYM>;
-            case 32: return k_skinny<2, SYM>;
-            case 48: return k_skinny<3, SYM>;
-            case 64: return k_skinny<4, SYM>;
-        }
-    } else if (path == kGemv) {
-        switch (mrows) {
-            case 1: return k_gemv<1, SYM>;
-            case 2: return k_gemv<2, SYM>;
-            case 3: return k_gemv<3, SYM>;
-            case 4: return k_gemv<4, SYM>;
-            case 5: return k_gemv<5, SYM>;
-            case 6: return k_gemv<6, SYM>;
-            case 7: return k_gemv<7, SYM>;
-            case 8: return k_gemv<8, SYM>;
-        }
+static FwdKernel pick(int kern, int mrows) {
+    switch (kern) {
+        case kKernMfma16:
+            return k_mfma16<SYM>;
+        case kKernGemv:
+            switch (mrows) {
+                case 1: return k_gemv4<1, SYM>;
+                case 2: return k_gemv4<2, SYM>;
+                case 3: return k_gemv4<3, SYM>;
+                case 4: return k_gemv4<4, SYM>;
+            }
+            break;
+        case kKernStaged:
+            switch (mrows) {
+                case 16: return k_skinny<1, SYM>;
+                case 32: return k_skinny<2, SYM>;
+                case 48: return k_skinny<3, SYM>;
+                case 64: return k_skinny<4, SYM>;
+            }
+            break;
     }
     return nullptr;
 }
 
-static FwdKernel pick_kernel(int path, int mrows, bool symmetric) {
-    return symmetric ? pick<true>(path, mrows) : pick<false>(path, mrows);
+static FwdKernel pick_kernel(int kern, int mrows, bool symmetric) {
+    return symmetric ? pick<true>(kern, mrows) : pick<false>(kern, mrows);
 }
 
-const char *kernel_name(int path, int mrows, bool symmetric) {
-    static const char *sk[2][4] = {{"k_skinny<1>", "k_skinny<2>", "k_skinny<3>", "k_skinny<4>"},
-                                   {"k_skinny<1,sym>", "k_skinny<2,sym>", "k_skinny<3,sym>", "k_skinny<4,sym>"}};
-    static const char *gv[2][8] = {{"k_gemv<1>", "k_gemv<2>", "k_gemv<3>", "k_gemv<4>", "k_gemv<5>",
-                                    "k_gemv<6>", "k_gemv<7>", "k_gemv<8>"},
-                                   {"k_gemv<1,sym>", "k_gemv<2,sym>", "k_gemv<3,sym>", "k_gemv<4,sym>",
-                                    "k_gemv<5,sym>", "k_gemv<6,sym>", "k_gemv<7,sym>", "k_gemv<8,sym>"}};
-    if (path == kSkinny && mrows % 16 == 0 && mrows >= 16 && mrows <= 64) return sk[symmetric][mrows / 16 - 1];
-    if (path == kGemv && mrows >= 1 && mrows <= 8) return gv[symmetric][mrows - 1];
-    return "?";
+const char *kernel_name(int kern, int mrows, bool symmetric) {
+    static char buf[64];
+    if (kern == kKernMfma16) snprintf(buf, sizeof buf, "k_mfma16%s", symmetric ? "<sym>" : "");
+    else if (kern == kKernGemv) snprintf(buf, sizeof buf, "k_gemv4<%d%s>", mrows, symmetric ? ",sym" : "");
+    else snprintf(buf, sizeof buf, "k_skinny<%d%s>", mrows / 16, symmetric ? ",sym" : "");
+    return buf;
 }
 
 hipError_t prepare_kernels() {
     for (int sym = 0; sym < 2; ++sym) {
-        for (int mr = 16; mr <= 64; mr += 16) {
-            hipError_t e = hipFuncSetAttribute((const void *)pick_kernel(kSkinny, mr, sym),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
-            if (e != hipSuccess) return e;
-        }
-        for (int mv = 1; mv <= 8; ++mv) {
-            hipError_t e = hipFuncSetAttribute((const void *)pick_kernel(kGemv, mv, sym),
-                                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
-            if (e != hipSuccess) return e;
-        }
+        (void)hipFuncSetAttribute((const void *)pick_kernel(kKernMfma16, 16, sym),
+                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
+        for (int mv = 1; mv <= kMaxGemvM; ++mv)
+            (void)hipFuncSetAttribute((const void *)pick_kernel(kKernGemv, mv, sym),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
+        for (int mr = 16; mr <= 64; mr += 16)
+            (void)hipFuncSetAttribute((const void *)pick_kernel(kKernStaged, mr, sym),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
     }
     return hipSuccess;
 }
 
-hipError_t launch_forward(int path, int mrows, bool symmetric, int grid, size_t lds,
+hipError_t launch_forward(int kern, int mrows, bool symmetric, int grid, size_t lds,
                           const FwdArgs &a, hipStream_t st) {
-    FwdKernel k = pick_kernel(path, mrows, symmetric);
+    FwdKernel k = pick_kernel(kern, mrows, symmetric);
     if (!k) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k, dim3(grid), dim3(kThreads), lds, st, a);
     return hipGetLastError();

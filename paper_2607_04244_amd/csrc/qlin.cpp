@@ -34,7 +34,6 @@ struct qlin_s {
 namespace {
 
 constexpr int kWsRowsMin = 128;        // S * M always allowed by the partial-sum workspace
-constexpr size_t kXLdsBudget = 128 * 1024;   // LDS for the staged x chunk (rest: accumulators)
 constexpr int64_t kMaxK = 65536, kMaxN = 1 << 20, kMaxM = 65536;
 
 thread_local char g_err[512] = "";
@@ -106,6 +105,18 @@ int check_zeros(const uint16_t *z, size_t n) {
     return QLIN_OK;
 }
 
+// Does a K chunk of Kc groups fit one workgroup (staged x + one column tile)?
+bool chunk_fits(int path, int rows, int Kc) {
+    return x_chunks(rows, Kc) <= kXChunksMax && lds_bytes(path, rows, Kc, 1) <= kLdsMax;
+}
+
+// Smallest number of K chunks whose chunks fit a workgroup.
+int min_split(int path, int rows, int Kb) {
+    for (int S = 1; S <= Kb; ++S)
+        if (chunk_fits(path, rows, (Kb + S - 1) / S)) return S;
+    return Kb + 1;   // not even one group fits (cannot happen for rows <= 64)
+}
+
 void free_handle(qlin_s *h) {
     if (!h) return;
     if (h->codes) (void)hipFree(h->codes);
@@ -136,12 +147,14 @@ qlin_t create_impl(int64_t K, int64_t N, int64_t group, const uint32_t *packed, 
     const size_t code_bytes = (size_t)N * K / 2;
     const size_t sz_bytes = ngroups * (symmetric ? 2 : 4);
     h->counters_n = std::max(h->Nt, 1);
-    // rows of partial sums the smallest feasible K split needs for each m-tile count
+    // rows of partial sums the smallest feasible K split needs, for every
+    // row count a kernel template can be launched with
     h->ws_rows = kWsRowsMin;
-    for (int mt = 1; mt <= kMaxSkinnyM / 16; ++mt) {
-        const int kc_max = (int)(kXLdsBudget / ((size_t)16 * mt * 256));
-        const int s_min = (h->Kb + kc_max - 1) / kc_max;
-        if (s_min > 1) h->ws_rows = std::max(h->ws_rows, s_min * 16 * mt);
+    for (int rows = 1; rows <= kMaxSkinnyM; ++rows) {
+        const bool gemv = rows <= kMaxGemvM;
+        if (!gemv && rows % 16) continue;
+        const int s_min = min_split(gemv ? kGemv : kSkinny, rows, h->Kb);
+        if (s_min > 1) h->ws_rows = std::max(h->ws_rows, s_min * rows);
     }
 
     void *canon = nullptr, *sc = nullptr, *zc = nullptr;
@@ -190,12 +203,13 @@ qlin_t create_impl(int64_t K, int64_t N, int64_t group, const uint32_t *packed, 
 
 struct Plan {
     int path = 0;
-    int mrows = 0;     // template row count (GEMV: M; SKINNY: 16 * m-tiles)
+    int kern = 0;
+    int mrows = 0;     // template row count (GEMV: M; MFMA kernels: 16 * m-tiles)
     int S = 1, Gn = 1, grid = 1;
     size_t lds = 0;
 };
 
-// Auto M-dispatch: vector-ALU GEMV up to this M, matrix-core SKINNY above.
+// Auto M-dispatch: vector-ALU GEMV up to this M, matrix cores above.
 int gemv_max_auto() {
     static int v = [] {
         const char *e = getenv("QLIN_GEMV_MAX_M");
@@ -204,10 +218,19 @@ int gemv_max_auto() {
     return v;
 }
 
+// M <= 16: register-resident group-major kernel (QLIN_KERN16=regs) or the
+// LDS-staged tile-major kernel (default).
+bool use_regs16() {
+    static bool v = [] {
+        const char *e = getenv("QLIN_KERN16");
+        return e && strcmp(e, "regs") == 0;
+    }();
+    return v;
+}
+
 // Cost (ns) of a (S, Gn) split: the slowest workgroup's share of HBM time,
-// the activation staging it does first, and the partial-sum traffic + arrival
-// fix-up when the K range is cut (S > 1).
-double plan_cost(const qlin_s *h, int path, int mrows, int M, int S, int Gn) {
+// plus the partial-sum traffic and arrival fix-up when the K range is cut.
+double plan_cost(const qlin_s *h, int M, int S, int Gn) {
     const double bw = 6.0e3;                          // bytes per ns, sustained HBM read
     const double per_cu = bw / h->num_cu;
     const int Kc = (h->Kb + S - 1) / S, Tn = (h->Nt + Gn - 1) / Gn;
@@ -216,9 +239,7 @@ double plan_cost(const qlin_s *h, int path, int mrows, int M, int S, int Gn) {
     const double blk = 1024.0 + (h->symmetric ? 32.0 : 64.0);
     const double wg_bytes = (double)Tn * Kc * blk;
     double t = std::max(rounds * wg_bytes / per_cu, (double)h->Nt * h->Kb * blk / bw);
-    const int xrows = (path == kGemv) ? M : mrows;
-    t += rounds * (double)Kc * xrows * 256.0 / 100.0;   // ~100 B/ns per CU from L2 into LDS
-    if (S > 1) t += 2.0 * S * M * (double)h->N * 4.0 / bw + 1500.0;
+    if (S > 1) t += 2.0 * S * M * (double)h->N * 4.0 / bw + 3000.0;
     return t;
 }
 
@@ -226,25 +247,44 @@ int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
     if (path == kAuto) path = (M <= gemv_max_auto()) ? kGemv : kSkinny;
     if (path == kTiled) path = kSkinny;   // prefill-sized M is run in 64-row slices for now
     if (path != kGemv && path != kSkinny) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
-    if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= 8");
+    if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= %d", kMaxGemvM);
+    if (split_k < 0 || split_k > h->Kb) return fail(QLIN_ERR_INVALID, "split_k must be in [0, K/128]");
     const int Mi = (int)std::min<int64_t>(M, kMaxSkinnyM);
     p->path = path;
-    p->mrows = (path == kGemv) ? Mi : 16 * ((Mi + 15) / 16);
+    int tn_max;
+    if (path == kGemv) {
+        p->kern = kKernGemv;
+        p->mrows = Mi;
+        tn_max = kTnMaxGemv;
+    } else if (Mi <= 16 && use_regs16()) {
+        p->kern = kKernMfma16;
+        p->mrows = 16;
+        tn_max = kTnMax;
+    } else {
+        p->kern = kKernStaged;
+        p->mrows = 16 * ((Mi + 15) / 16);
+        tn_max = h->Nt;
+    }
+    const bool regs = p->kern != kKernStaged;
     const int rows = p->mrows;
-    if (split_k < 0 || split_k > h->Kb) return fail(QLIN_ERR_INVALID, "split_k must be in [0, K/128]");
+    const int gn_min = (h->Nt + tn_max - 1) / tn_max;
 
     auto fits = [&](int S, int Gn) {
         const int Kc = (h->Kb + S - 1) / S, Tn = (h->Nt + Gn - 1) / Gn;
         if (S > 1 && S * Mi > h->ws_rows) return false;
-        if (Gn > h->counters_n) return false;
-        return lds_bytes(path, rows, Kc, Tn) <= kLdsMax;
+        if (Gn > h->counters_n || Tn > tn_max) return false;
+        if (regs) return lds_bytes_regs(rows) <= kLdsMax;
+        if (!chunk_fits(kSkinny, rows, Kc)) return false;
+        return lds_bytes(kSkinny, rows, Kc, Tn) <= kLdsMax;
     };
-    auto gn_for = [&](int S) { return std::max(1, std::min(h->Nt, (int)std::lround((double)h->num_cu / S))); };
+    auto gn_for = [&](int S) {
+        return std::max(gn_min, std::min(h->Nt, (int)std::lround((double)h->num_cu / S)));
+    };
 
     int bestS = -1, bestGn = 1;
     if (split_k > 0) {
         const int S = (int)split_k;
-        int Gn = gn_for(S);
+        int Gn = std::min(gn_for(S), h->Nt);
         while (Gn < h->Nt && !fits(S, Gn)) ++Gn;
         if (!fits(S, Gn)) return fail(QLIN_ERR_UNSUPPORTED, "split_k=%d does not fit (LDS or workspace)", S);
         bestS = S;
@@ -252,10 +292,10 @@ int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
     } else {
         double best = 1e300;
         for (int S = 1; S <= std::min(h->Kb, 64); ++S) {
-            int Gn = gn_for(S);
+            int Gn = std::min(gn_for(S), h->Nt);
             while (Gn < h->Nt && !fits(S, Gn)) ++Gn;
             if (!fits(S, Gn)) continue;
-            const double c = plan_cost(h, path, rows, Mi, S, Gn);
+            const double c = plan_cost(h, Mi, S, Gn);
             if (c < best) { best = c; bestS = S; bestGn = Gn; }
         }
         if (bestS < 0) return fail(QLIN_ERR_UNSUPPORTED, "no work split fits this shape");
@@ -264,9 +304,10 @@ int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
     p->Gn = bestGn;
     p->grid = bestS * bestGn;
     const int Kc = (h->Kb + bestS - 1) / bestS, Tn = (h->Nt + bestGn - 1) / bestGn;
+    const size_t need = regs ? lds_bytes_regs(rows) : lds_bytes(kSkinny, rows, Kc, Tn);
     // at least 80 KiB + 1 of LDS per workgroup keeps one workgroup per CU, so
     // the grid spreads over all CUs
-    p->lds = std::max(lds_bytes(path, rows, Kc, Tn), (size_t)80 * 1024 + 256);
+    p->lds = std::max(need, (size_t)80 * 1024 + 256);
     return QLIN_OK;
 }
 
@@ -288,7 +329,7 @@ int run_forward(qlin_s *h, int path, int64_t split_k, int64_t M, const uint16_t 
     int rc = check_forward_args(h, M, x, y);
     if (rc != QLIN_OK || M == 0) return rc;
     if (path == kSkinny && M > kMaxSkinnyM) return fail(QLIN_ERR_UNSUPPORTED, "SKINNY path needs M <= 64");
-    if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= 8");
+    if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= %d", kMaxGemvM);
     if (path < kAuto || path > kTiled) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
     int dev = -1;
     hipError_t e = hipGetDevice(&dev);
@@ -315,7 +356,11 @@ int run_forward(qlin_s *h, int path, int64_t split_k, int64_t M, const uint16_t 
         a.Nt = h->Nt;
         a.S = p.S;
         a.Gn = p.Gn;
-        e = launch_forward(p.path, p.mrows, h->symmetric, p.grid, p.lds, a, st);
+        a.Nq = h->Nt / p.Gn;
+        a.Nr = h->Nt % p.Gn;
+        a.Kq = h->Kb / p.S;
+        a.Kr = h->Kb % p.S;
+        e = launch_forward(p.kern, p.mrows, h->symmetric, p.grid, p.lds, a, st);
         if (e != hipSuccess) return hip_fail(e, "forward launch");
     }
     return QLIN_OK;
@@ -354,14 +399,14 @@ int qlin_plan(qlin_t h, int path, int64_t split_k, int64_t M, char *buf, int64_t
     if (!buf || buflen <= 0) return fail(QLIN_ERR_INVALID, "NULL buffer");
     if (M <= 0 || M > kMaxM) return fail(QLIN_ERR_INVALID, "M must be in [1, 65536]");
     if (path < kAuto || path > kTiled) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
-    if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= 8");
+    if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= %d", kMaxGemvM);
     if (path == kSkinny && M > kMaxSkinnyM) return fail(QLIN_ERR_UNSUPPORTED, "SKINNY path needs M <= 64");
     Plan p;
     int rc = make_plan(h, path, split_k, std::min<int64_t>(M, kMaxSkinnyM), &p);
     if (rc != QLIN_OK) return rc;
     const int64_t slices = (M + kMaxSkinnyM - 1) / kMaxSkinnyM;
     snprintf(buf, (size_t)buflen, "path=%s kernel=%s grid=%d block=%d split=%d ranges=%d lds=%zu launches=%lld",
-             p.path == kGemv ? "gemv" : "skinny", kernel_name(p.path, p.mrows, h->symmetric), p.grid, kThreads,
+             p.path == kGemv ? "gemv" : "skinny", kernel_name(p.kern, p.mrows, h->symmetric), p.grid, kThreads,
              p.S, p.Gn, p.lds, (long long)slices);
     return QLIN_OK;
 }
