@@ -1,7 +1,7 @@
 """Benchmark of the W4A16 linear layer on one MI355X.
 
-Workload: the draft-block verification linear, M = 16 rows (one 16-token
-draft block), K = 2560, N = 19456 (fused gate + up projection of a
+Default workload: the draft-block verification linear, M = 16 rows (one
+16-token draft block), K = 2560, N = 19456 (fused gate + up projection of a
 4B-shaped decoder), int4 codes with bf16 scales and zero-points in groups of
 128 along K.  A step is one qlin_forward of that linear: activation staging,
 weight streaming, dequantization, the dot products and the reduction, all in
@@ -11,10 +11,17 @@ like loading a model).
 To measure HBM rather than the 256 MB last-level cache, R handles with their
 own copies of the weights (over 1 GiB together) are used in turn, and the
 steps are replayed from a HIP graph so host launch cost is not measured.
+The same rotation is timed for a plain 128-bit streaming read of the same
+byte count (qlin_stream_read), the achievable ceiling at this size.
 
 Prints one JSON line.  ``value`` is algorithmic bytes per step / time per step
 (GB/s); the algorithmic bytes are the int4 codes, the bf16 scales and zeros,
 x and y (K*N/2 + 4*(K/128)*N + 2*M*K + 2*M*N).
+
+Other modes (not the benchmark line): ``--workload`` c0 | c2m1 | c2m4 |
+c2m8 | c2m16 | model (36 layers x 6 linears at M=16, microseconds per
+verification step); ``--calibrate-copy`` runs a plain 256 MiB device copy for
+the HBM-traffic counter calibration.
 """
 
 import argparse
@@ -57,8 +64,8 @@ def traffic_from_profiles(kernel_src_hash, kernel):
     return None if e is None else e.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(case, budget_s=15.0):
-    """Time the oracle (as it stands) on the host cores on whole config-1 calls."""
+def cpu_baseline(case, budget_s=12.0):
+    """Time the oracle (as it stands) on the host cores on whole calls."""
     from oracle import qlin_ref as ref
     try:
         from threadpoolctl import threadpool_info
@@ -67,18 +74,105 @@ def cpu_baseline(case, budget_s=15.0):
         threads = 1
     times = []
     t_start = time.perf_counter()
-    while True:
+    while time.perf_counter() - t_start < budget_s and len(times) < 50:
         t0 = time.perf_counter()
         ref.forward(case["x"], case["packed"], case["scales"], case["zeros"])
         times.append(time.perf_counter() - t0)
-        if time.perf_counter() - t_start > budget_s or len(times) >= 5:
-            break
     t = float(np.median(times))
     b = algorithmic_bytes(case["M"], case["K"], case["N"])
     return {"value": round(b / t / 1e9, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{len(times)} whole oracle calls of the M=16 K=2560 N=19456 linear "
-                      f"(median {t:.2f} s each; numpy unpack/dequant single-threaded, fp64 matmul on "
-                      f"{threads} BLAS threads)"}
+            "sample": f"{len(times)} whole oracle calls of the M={case['M']} K={case['K']} N={case['N']} "
+                      f"linear (median {t:.3f} s each; numpy unpack/dequant single-threaded, fp64 "
+                      f"matmul on {threads} BLAS threads)"}
+
+
+def graph_time_us(torch, stream, launches, reps):
+    """Capture `launches` (list of callables) in one graph; median us per launch."""
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        for f in launches:
+            f()
+    g.replay()
+    stream.synchronize()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    with torch.cuda.stream(stream):
+        ev0.record(stream)
+        for _ in range(reps):
+            g.replay()
+        ev1.record(stream)
+    stream.synchronize()
+    return ev0.elapsed_time(ev1) * 1e3 / (reps * len(launches)), g
+
+
+def stream_read_ceiling(torch, qlin, nbytes, stream):
+    """Plain streaming read of nbytes per launch over > 1 GiB of rotating buffers."""
+    R = max(2, -(-(1 << 30) // nbytes))
+    nb = (nbytes + 15) // 16 * 16
+    bufs = [torch.empty(nb, dtype=torch.uint8, device="cuda").fill_(i & 0xFF) for i in range(R)]
+    sink = torch.zeros(4096, dtype=torch.int32, device="cuda")
+    best = None
+    for grid in (512, 1024, 2048):
+        def mk(b):
+            return lambda: qlin.qlin_stream_read(b.data_ptr(), nb, grid, sink.data_ptr(), stream.cuda_stream)
+        us, _ = graph_time_us(torch, stream, [mk(b) for b in bufs], reps=max(3, int(4e9 / (nb * R))))
+        best = us if best is None else min(best, us)
+    del bufs
+    return nb / (best * 1e-6) / 1e9, best
+
+
+def make_case(workload):
+    from synth import gen
+    if workload == "verify":
+        return gen.linear_case(1)
+    if workload == "c0":
+        return gen.linear_case(0)
+    if workload.startswith("c2m"):
+        return gen.linear_case(2, M=int(workload[3:]))
+    raise ValueError(workload)
+
+
+def calibrate_copy():
+    """A plain device-to-device copy of 256 MiB, 20 times (counter calibration:
+    each launch reads and writes exactly 268,435,456 bytes)."""
+    import torch
+    torch.cuda.set_device(0)
+    a = torch.ones(1 << 28, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(20):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "device copy", "bytes_read_per_launch": 1 << 28,
+                      "bytes_written_per_launch": 1 << 28, "launches": 20}), flush=True)
+
+
+def bench_model(args):
+    """36 layers x (q, k, v, o, gate_up, down) at M=16: one graph per step."""
+    import torch
+
+    from paper_2607_04244_amd import qlin
+    from synth import gen
+    torch.cuda.set_device(0)
+    M = 16
+    lins, xs, ys, total = [], {}, [], 0
+    for layer in range(gen.N_LAYERS):
+        for p in range(len(gen.LAYER_SHAPES)):
+            w = gen.model_linear(layer, p)
+            lins.append(qlin.QLinear(w["packed"], w["scales"], w["zeros"]))
+            K, N = w["K"], w["N"]
+            if K not in xs:
+                xs[K] = torch.from_numpy(gen.model_activations(3, M, K).view(np.int16)).view(torch.bfloat16).cuda()
+            ys.append(torch.empty((M, N), dtype=torch.bfloat16, device="cuda"))
+            total += algorithmic_bytes(M, K, N)
+    stream = torch.cuda.Stream()
+    calls = [(lambda l=l, y=y: l.forward(xs[l.K], out=y)) for l, y in zip(lins, ys)]
+    us_per_launch, g = graph_time_us(torch, stream, calls, reps=max(1, args.steps // 216))
+    us_step = us_per_launch * len(calls)
+    out = {"workload": "36-layer 4B decoder weight pass M=16 (216 linears, one graph)",
+           "us_per_step": round(us_step, 2), "us_per_layer": round(us_step / gen.N_LAYERS, 3),
+           "bytes_per_step": total, "GBps": round(total / (us_step * 1e-6) / 1e9, 1),
+           "pct_of_peak_hbm": round(100 * total / (us_step * 1e-6) / 1e9 / PEAK_HBM_GBS, 2)}
+    print(json.dumps(out), flush=True)
 
 
 def main():
@@ -89,19 +183,24 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle timing")
     ap.add_argument("--path", type=int, default=0, help="force a kernel path (tuning)")
     ap.add_argument("--split", type=int, default=0, help="force a K split (tuning)")
+    ap.add_argument("--workload", default="verify")
+    ap.add_argument("--calibrate-copy", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the layer has no multi-GPU path in this build "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy:
+        return calibrate_copy()
+    if args.workload == "model":
+        return bench_model(args)
 
     import torch
 
     from paper_2607_04244_amd import qlin
-    from synth import gen
 
     torch.cuda.set_device(0)
-    case = gen.linear_case(1)
+    case = make_case(args.workload)
     M, K, N = case["M"], case["K"], case["N"]
     bytes_step = algorithmic_bytes(M, K, N)
     weight_bytes = K * N // 2 + 4 * (K // 128) * N
@@ -160,10 +259,17 @@ def main():
         ev3.record(stream)
     stream.synchronize()
     eager_us = ev2.elapsed_time(ev3) * 1e3 / n_eager
+    for l in lins:
+        l.close()
+    del lins
+    torch.cuda.empty_cache()
+    ceil_gbs, ceil_us = stream_read_ceiling(torch, qlin, bytes_step, stream)
 
     kernel = plan.split("kernel=")[1].split()[0] if "kernel=" in plan else "?"
     src_hash = file_hash(os.path.join(ROOT, "paper_2607_04244_amd", "csrc", "kernels.hip"))
     traffic = traffic_from_profiles(src_hash, kernel)
+    wl = {"verify": "draft-block verification linear: M=16, K=2560, N=19456 (fused gate+up)"}.get(
+        args.workload, f"{args.workload}: M={M}, K={K}, N={N}")
     out = {
         "metric": METRIC,
         "value": round(gbs, 2),
@@ -177,19 +283,18 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "draft-block verification linear: M=16, K=2560, N=19456 (fused gate+up), "
-                               "int4 g128 asymmetric, bf16 scales/zeros",
+        "config": {"workload": wl + ", int4 g128 asymmetric, bf16 scales/zeros",
                    "M": M, "K": K, "N": N, "group": 128, "rotating_weight_copies": R,
                    "bytes_per_step": bytes_step, "plan": plan, "timing": "HIP graph replay",
                    "us_per_step": round(ms_step * 1e3, 3), "pct_of_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2),
+                   "stream_read_ceiling_GBps": round(ceil_gbs, 1), "stream_read_ceiling_us": round(ceil_us, 3),
+                   "pct_of_stream_read_ceiling": round(100 * gbs / ceil_gbs, 1),
                    "eager_launch_us_per_step": round(eager_us, 3)},
         "roofline": {"bound": "hbm", "kernel": kernel, "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
                      "traffic": traffic, "bytes_per_launch": bytes_step,
                      "avg_launch_us": round(ms_step * 1e3, 3)},
     }
-    for l in lins:
-        l.close()
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(case)
     print(json.dumps(out), flush=True)

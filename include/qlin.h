@@ -145,6 +145,18 @@ int qlin_dequantize(qlin_t h, int routine, uint16_t *w_out, void *stream);
 /* qlin_shape -- K and N of a handle (either pointer may be NULL). */
 int qlin_shape(qlin_t h, int64_t *K, int64_t *N);
 
+/*
+ * qlin_stream_read -- measurement utility: the HBM read ceiling the layer is
+ * compared with.  Reads `bytes` bytes at `buf` (DEVICE, 16-byte aligned,
+ * bytes a multiple of 16) with 128-bit loads over `grid` workgroups of 512
+ * threads (grid <= 0: 4 per CU), 8 loads in flight per thread, and XOR-folds
+ * them; one uint32 per workgroup is written to `sink` (DEVICE, grid entries)
+ * only in the practically impossible case that the fold equals 0x12345678, so
+ * the traffic is reads only.  Asynchronous on stream.
+ * Errors: INVALID (NULL, bytes <= 0 or not a multiple of 16), ALIGN, HIP.
+ */
+int qlin_stream_read(const void *buf, int64_t bytes, int grid, uint32_t *sink, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -844,6 +844,35 @@ __global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
     write_out_waves(a, w, slots, MV);
 }
 
+// ------------------------------------------------------------------ measurement
+
+// Stream-read ceiling: 8 independent 128-bit loads in flight per thread,
+// XOR-folded; writes only if the fold hits an (in practice) impossible value.
+__global__ void __launch_bounds__(512) k_stream_read(const uint4 *__restrict__ p, size_t n16,
+                                                     uint32_t *__restrict__ sink) {
+    constexpr int U = 8;
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+    uint32_t acc = 0;
+    for (; i + (U - 1) * stride < n16; i += U * stride) {
+        uint4 v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = p[i + u * stride];
+#pragma unroll
+        for (int u = 0; u < U; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+    }
+    for (; i < n16; i += stride) {
+        const uint4 v = p[i];
+        acc ^= v.x ^ v.y ^ v.z ^ v.w;
+    }
+    if (acc == 0x12345678u) sink[blockIdx.x] = acc;
+}
+
+hipError_t launch_stream_read(const void *buf, size_t bytes, int grid, uint32_t *sink, hipStream_t st) {
+    hipLaunchKernelGGL(k_stream_read, dim3(grid), dim3(512), 0, st, (const uint4 *)buf, bytes / 16, sink);
+    return hipGetLastError();
+}
+
 // ------------------------------------------------------------------ host launchers
 
 static inline int grid_for(size_t items, int per_block) {

@@ -446,6 +446,23 @@ int qlin_dequantize(qlin_t h, int routine, uint16_t *w_out, void *stream) {
     return e == hipSuccess ? QLIN_OK : hip_fail(e, "dequantize launch");
 }
 
+int qlin_stream_read(const void *buf, int64_t bytes, int grid, uint32_t *sink, void *stream) {
+    clear_err();
+    if (!buf || !sink) return fail(QLIN_ERR_INVALID, "NULL argument");
+    if (bytes <= 0 || bytes % 16) return fail(QLIN_ERR_INVALID, "bytes must be a positive multiple of 16");
+    if ((uintptr_t)buf & 15) return fail(QLIN_ERR_ALIGN, "buf must be 16-byte aligned");
+    hipError_t e;
+    if (grid <= 0) {
+        int dev = 0, cus = 0;
+        if ((e = hipGetDevice(&dev)) != hipSuccess) return hip_fail(e, "hipGetDevice");
+        if ((e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+            return hip_fail(e, "hipDeviceGetAttribute");
+        grid = 4 * cus;
+    }
+    e = launch_stream_read(buf, (size_t)bytes, grid, sink, (hipStream_t)stream);
+    return e == hipSuccess ? QLIN_OK : hip_fail(e, "stream-read launch");
+}
+
 int qlin_shape(qlin_t h, int64_t *K, int64_t *N) {
     clear_err();
     if (!h) return fail(QLIN_ERR_INVALID, "NULL handle");

@@ -78,6 +78,7 @@ hipError_t launch_unpack(const uint4 *codes, uint8_t *q, int K, int N, hipStream
 hipError_t launch_dequant(int routine, const uint4 *codes, const void *sz, bool symmetric,
                           uint16_t *w, int K, int N, hipStream_t st);
 hipError_t prepare_kernels();     // per-process attribute setup (LDS limits)
+hipError_t launch_stream_read(const void *buf, size_t bytes, int grid, uint32_t *sink, hipStream_t st);
 const char *kernel_name(int kern, int mrows, bool symmetric);
 
 }  // namespace qlin

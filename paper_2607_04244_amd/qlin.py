@@ -26,7 +26,7 @@ PATH_AUTO, PATH_GEMV, PATH_SKINNY, PATH_TILED = 0, 1, 2, 3
 # every symbol include/qlin.h declares
 EXPORTS = ("qlin_create", "qlin_create_symmetric", "qlin_forward", "qlin_forward_path",
            "qlin_plan", "qlin_destroy", "qlin_last_error", "qlin_unpack_codes",
-           "qlin_dequantize", "qlin_shape", "qlin_last_status")
+           "qlin_dequantize", "qlin_shape", "qlin_last_status", "qlin_stream_read")
 
 _lib = None
 
@@ -66,6 +66,8 @@ def lib():
     L.qlin_unpack_codes.argtypes = [P, VP, VP]
     L.qlin_dequantize.restype = I32
     L.qlin_dequantize.argtypes = [P, I32, VP, VP]
+    L.qlin_stream_read.restype = I32
+    L.qlin_stream_read.argtypes = [VP, I64, I32, VP, VP]
     L.qlin_shape.restype = I32
     L.qlin_shape.argtypes = [P, ctypes.POINTER(I64), ctypes.POINTER(I64)]
     _lib = L
@@ -143,6 +145,10 @@ def qlin_unpack_codes(h, q_ptr, stream):
 
 def qlin_dequantize(h, routine, w_ptr, stream):
     return lib().qlin_dequantize(h, routine, w_ptr, stream)
+
+
+def qlin_stream_read(buf_ptr, nbytes, grid, sink_ptr, stream):
+    return lib().qlin_stream_read(buf_ptr, nbytes, grid, sink_ptr, stream)
 
 
 def qlin_shape(h):
