@@ -49,8 +49,9 @@ enum {
 enum {
     QLIN_PATH_AUTO = 0,
     QLIN_PATH_GEMV = 1,    /* vector-ALU dequantize + v_dot2 dot product, M <= 4 */
-    QLIN_PATH_SKINNY = 2,  /* matrix-core dequantize + MFMA 16x16x32, M <= 64 */
-    QLIN_PATH_TILED = 3    /* LDS-tiled MFMA GEMM for prefill-sized M */
+    QLIN_PATH_SKINNY = 2,  /* matrix-core dequantize + MFMA 16x16x32, x chunk staged in LDS, M <= 64 */
+    QLIN_PATH_TILED = 3,   /* LDS-tiled MFMA GEMM for prefill-sized M */
+    QLIN_PATH_REGS = 4     /* matrix-core dequantize + MFMA 16x16x32, x fragments in registers, M <= 16 */
 };
 
 /*
@@ -104,7 +105,8 @@ int qlin_forward(qlin_t h, int64_t M, const uint16_t *x, uint16_t *y, void *stre
  * K-chunks (split_k; 0 = the planner's choice) forced, for tests and tuning.
  * Errors as qlin_forward, plus INVALID for an unknown path, split_k < 0 or
  * split_k > K/128, and UNSUPPORTED when the path cannot run this M
- * (GEMV: M <= 4; SKINNY: M <= 64).
+ * (GEMV: M <= 4; REGS: M <= 16; SKINNY: M <= 64) or the forced split does
+ * not fit.
  */
 int qlin_forward_path(qlin_t h, int path, int64_t split_k, int64_t M,
                       const uint16_t *x, uint16_t *y, void *stream);

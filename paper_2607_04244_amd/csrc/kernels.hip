@@ -8,9 +8,9 @@
 // Device weight layout ("block layout").  The canonical [N][K/8] words are
 // re-laid-out at handle creation into blocks of 16 columns x 128 k (one
 // quantization group of one column tile) = 256 words = 1 KiB.  Block (t, kb)
-// starts at word (kb * Nt + t) * 256 (Nt = N / 16 tiles): the blocks of one
-// group for consecutive column tiles are consecutive KiB, which is the order
-// the forward kernels stream them in.  Lane l of a wave owns words
+// starts at word (t * Kb + kb) * 256 (Kb = K / 128 groups): the K range of a
+// column tile is one contiguous run of KiB blocks, so a wave that walks a
+// tile's groups reads memory sequentially.  Lane l of a wave owns words
 // [4l, 4l + 4) of a block (one 128-bit load); word j of lane l covers k in
 // [32j, 32j + 32) of the group, and its nibble p holds the code of
 //     n = 16 t + 4 * ((l >> 2) & 3) + r,   r  = 2 * (p & 1) + (p >> 2)
@@ -186,8 +186,7 @@ __global__ void k_repack_codes(const uint32_t *__restrict__ canon, uint32_t *__r
         const size_t b = idx / kBlockU32;
         const int within = (int)(idx % kBlockU32);
         const int l = within >> 2, j = within & 3;
-        const int Nt = N / kTileN;
-        const int kb = (int)(b / Nt), t = (int)(b % Nt);
+        const int t = (int)(b / Kb), kb = (int)(b % Kb);     // block b = t * Kb + kb
         uint32_t word = 0;
         for (int p = 0; p < 8; ++p) {
             int n16, k128;
@@ -207,9 +206,8 @@ __global__ void k_repack_sz(const uint16_t *__restrict__ scales, const uint16_t 
     for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
          idx += (size_t)gridDim.x * blockDim.x) {
         const int n16 = (int)(idx % kTileN);
-        const size_t tb = idx / kTileN;               // kb * Nt + t
-        const int Nt = N / kTileN;
-        const int kb = (int)(tb / Nt), t = (int)(tb % Nt);
+        const size_t tb = idx / kTileN;               // block t * Kb + kb
+        const int t = (int)(tb / Kb), kb = (int)(tb % Kb);
         const size_t n = (size_t)t * kTileN + n16;
         const uint16_t s = scales[n * Kb + kb];
         if (symmetric) {
@@ -230,7 +228,7 @@ __global__ void k_unpack(const uint4 *__restrict__ codes, uint8_t *__restrict__ 
          b += (size_t)gridDim.x * (blockDim.x >> 6)) {
         const uint4 c = codes[b * 64 + l];
         const uint32_t w[4] = {c.x, c.y, c.z, c.w};
-        const int kb = (int)(b / (N / kTileN)), t = (int)(b % (N / kTileN));
+        const int t = (int)(b / Kb), kb = (int)(b % Kb);
         for (int j = 0; j < 4; ++j)
             for (int p = 0; p < 8; ++p) {
                 int n16, k128;
@@ -253,7 +251,7 @@ __global__ void k_dequant_mfma(const uint4 *__restrict__ codes, const void *__re
         const uint4 c = codes[b * 64 + l];
         const MfmaDeq d = mfma_setup(load_sz<SYM>(sz, b * kTileN + (l & 15)), shift, keep_lo);
         const uint32_t P[4] = {c.x, c.y, c.z, c.w};
-        const int kb = (int)(b / (N / kTileN)), t = (int)(b % (N / kTileN));
+        const int t = (int)(b / Kb), kb = (int)(b % Kb);
         const size_t n = (size_t)t * kTileN + (l & 15);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -282,7 +280,7 @@ __global__ void k_dequant_valu(const uint4 *__restrict__ codes, const void *__re
         for (int r = 0; r < 4; ++r) s4[r] = load_sz<SYM>(sz, b * kTileN + 4 * b2 + r);
         const ValuDeq d = valu_setup(s4);
         const uint32_t P[4] = {c.x, c.y, c.z, c.w};
-        const int kb = (int)(b / (N / kTileN)), t = (int)(b % (N / kTileN));
+        const int t = (int)(b / Kb), kb = (int)(b % Kb);
         for (int j = 0; j < 4; ++j) {
             uint32_t pr[4];
             valu_dequant(P[j], d, kx, pr);
@@ -320,53 +318,94 @@ __device__ inline void wave_range(int U, int i, int &u0, int &u1) {
 }
 
 // Walks the blocks of a wave's range in tile-major order u = tl * Kc + kbl:
-// block index (g0 + kbl) * Nt + t0 + tl and position (tile tl, group kbl)
-// within the workgroup's work, no division.
+// block index (t0 + tl) * Kb + g0 + kbl (consecutive blocks of a tile are
+// adjacent in memory) and position (tile tl, group kbl) within the
+// workgroup's work, no division.
 struct BlockWalk {
     int tl, kbl;
     size_t b;
-    __device__ inline void start(const WgWork &w, int Nt, int u) {
+    __device__ inline void start(const WgWork &w, int Kb, int u) {
         tl = 0;
         kbl = u;
         while (kbl >= w.Kc) { kbl -= w.Kc; ++tl; }   // u < Tn * Kc: at most Tn steps, once
-        b = (size_t)(w.g0 + kbl) * Nt + w.t0 + tl;
+        b = (size_t)(w.t0 + tl) * Kb + w.g0 + kbl;
     }
-    __device__ inline void next(const WgWork &w, int Nt) {
-        if (++kbl == w.Kc) { kbl = 0; ++tl; b -= (size_t)(w.Kc - 1) * Nt - 1; }
-        else b += Nt;
+    __device__ inline void next(const WgWork &w, int Kb) {
+        if (++kbl == w.Kc) { kbl = 0; ++tl; b += (size_t)(Kb - w.Kc) + 1; }
+        else ++b;
     }
 };
+
+// Split-K partial sums travel between workgroups that may sit on different
+// XCDs, whose L2 caches are not coherent with each other for ordinary
+// accesses.  They are written and read with agent-scope (sc1) buffer
+// accesses, which the hardware performs at the device coherence point; an
+// agent-scope release/acquire fence instead would write back and invalidate
+// the whole L2 of the XCD on every arrival.  Workgroup (c, jn) owns a
+// contiguous region of TnMax * M * 16 fp32 at ((c * Gn + jn) * TnMax * M * 16),
+// item it = (tile * M + m) * 2 + half at float offset 8 * it, so the 16-byte
+// accesses of a wave are contiguous.
+constexpr int kSc1 = 16;   // cache-policy operand of the buffer builtins: sc1 (agent scope)
+
+__device__ inline __amdgpu_buffer_rsrc_t ws_rsrc(const FwdArgs &a) {
+    return __builtin_amdgcn_make_buffer_rsrc(a.ws, 0, (int)a.ws_bytes, 0x00020000);
+}
+__device__ inline uint32_t ws_region(const FwdArgs &a, int c, int jn) {      // byte offset
+    return (uint32_t)((c * a.Gn + jn) * a.TnMax * a.M) * 64u;
+}
+__device__ inline void store_partial8(const FwdArgs &a, const WgWork &w, int it, const float s[8]) {
+    const __amdgpu_buffer_rsrc_t r = ws_rsrc(a);
+    const uint32_t off = ws_region(a, w.c, w.jn) + (uint32_t)it * 32u;
+    __builtin_amdgcn_raw_buffer_store_b128(v4u{__float_as_uint(s[0]), __float_as_uint(s[1]), __float_as_uint(s[2]),
+                                               __float_as_uint(s[3])}, r, off, 0, kSc1);
+    __builtin_amdgcn_raw_buffer_store_b128(v4u{__float_as_uint(s[4]), __float_as_uint(s[5]), __float_as_uint(s[6]),
+                                               __float_as_uint(s[7])}, r, off + 16, 0, kSc1);
+}
 
 // The last of the S workgroups of a column range adds the S fp32 partials in
 // chunk order (fixed order) and writes y.
 __device__ inline void reduce_chunks(const FwdArgs &a, const WgWork &w) {
     const int tid = threadIdx.x;
     const int items = w.Tn * a.M * 2;
-    // Publish: the barrier completes every wave's partial-sum stores (to L2);
-    // one agent-scope acq_rel atomic then writes the L2 back before counting
-    // this arrival and, for the last arrival, invalidates the caches so the
-    // other workgroups' partials are read fresh.  One fence per workgroup,
-    // not one per thread.
+    // Every wave waits until its partial-sum stores have completed at the
+    // device coherence point before the barrier; one relaxed atomic per
+    // workgroup then counts the arrival.  The last arrival reads the other
+    // workgroups' partials with agent-scope loads, which do not hit stale
+    // cached copies.
     __shared__ int s_last;
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     if (tid == 0) {
-        const uint32_t old = __hip_atomic_fetch_add(&a.counters[w.jn], 1u, __ATOMIC_ACQ_REL,
+        const uint32_t old = __hip_atomic_fetch_add(&a.counters[w.jn], 1u, __ATOMIC_RELAXED,
                                                     __HIP_MEMORY_SCOPE_AGENT);
         s_last = (old == (uint32_t)(a.S - 1));
     }
     __syncthreads();
     if (!s_last) return;
+    const __amdgpu_buffer_rsrc_t r = ws_rsrc(a);
     for (int it = tid; it < items; it += blockDim.x) {
         const int tl = it / (a.M * 2);
         const int rem = it - tl * a.M * 2;
         const int m = rem >> 1, hh = rem & 1;
         const size_t n = (size_t)(w.t0 + tl) * kTileN + 8 * hh;
+        // partials of kBatch chunks are loaded together (one memory round
+        // trip per batch, not per chunk), then added in chunk order
+        constexpr int kBatch = 8;
         float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-        for (int cc = 0; cc < a.S; ++cc) {
-            const float4 *src = (const float4 *)(a.ws + ((size_t)cc * a.M + m) * a.N + n);
-            const float4 v0 = src[0], v1 = src[1];
-            s[0] += v0.x; s[1] += v0.y; s[2] += v0.z; s[3] += v0.w;
-            s[4] += v1.x; s[5] += v1.y; s[6] += v1.z; s[7] += v1.w;
+        for (int c0 = 0; c0 < a.S; c0 += kBatch) {
+            v4u v[kBatch][2];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int cc = min(c0 + u, a.S - 1);      // unconditional load; extra ones are not added
+                const uint32_t off = ws_region(a, cc, w.jn) + (uint32_t)it * 32u;
+                v[u][0] = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kSc1);
+                v[u][1] = __builtin_amdgcn_raw_buffer_load_b128(r, off + 16, 0, kSc1);
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u)
+                if (c0 + u < a.S)
+#pragma unroll
+                    for (int i = 0; i < 8; ++i) s[i] += __uint_as_float(v[u][i >> 2][i & 3]);
         }
         uint4 o;
         o.x = cvt_pk_bf16(s[0], s[1]);
@@ -414,9 +453,7 @@ __device__ inline void write_out(const FwdArgs &a, const WgWork &w, const float 
             o.w = cvt_pk_bf16(s[6], s[7]);
             *(uint4 *)(a.y + (size_t)m * a.N + n) = o;
         } else {
-            float4 *dst = (float4 *)(a.ws + ((size_t)w.c * a.M + m) * a.N + n);
-            dst[0] = make_float4(s[0], s[1], s[2], s[3]);
-            dst[1] = make_float4(s[4], s[5], s[6], s[7]);
+            store_partial8(a, w, it, s);
         }
     }
     if (!direct) reduce_chunks(a, w);
@@ -459,11 +496,13 @@ struct StageWalk {
 // LDS slot; write_out() adds them in a fixed order.
 //
 // x in LDS: 16-byte fragments, fragment (kbl, c, row) = x[row][k0 .. k0 + 8)
-// with k0 = 128(g0 + kbl) + 8c, c = 4j + g < 16, stored at slot
-// (16 kbl + c) * MR + (row & ~15) + ((row & 15) ^ c).  The XOR swizzle keeps
-// both the staging writes (16 lanes = 16 consecutive c of one row) and the
-// operand reads (16 lanes = 16 rows of one c) on distinct LDS banks.  Lane l
-// of m-tile mt reads c = 4j + (l >> 4), row 16 mt + (l & 15).
+// with k0 = 128(g0 + kbl) + 8c, c = 4j + g < 16, for rows < M only, stored
+// at slot (16 kbl + c) * XR + (row & ~msk) + ((row ^ c) & msk), where XR =
+// staged_rows(M) (1, 2, 4, 8, 16 or 16 * MT) and msk = min(XR, 16) - 1.  The
+// XOR swizzle keeps both the staging writes (16 lanes = 16 consecutive c of
+// one row) and the operand reads (16 lanes = 16 rows of one c) on distinct
+// LDS banks.  Lane l of m-tile mt reads c = 4j + (l >> 4) of row
+// min(16 mt + (l & 15), M - 1).
 template <int MT, bool SYM>
 __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
@@ -472,8 +511,12 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: keeps the walk on the scalar unit
     const ExtractConsts kx;
     const WgWork w = wg_work(a, blockIdx.x);
+    // staged rows: next power of two >= M for one m-tile, else MR
+    int XR = MR;
+    if (MT == 1) { XR = 1; while (XR < a.M) XR <<= 1; }
+    const int msk = min(XR, 16) - 1;
     uint4 *xs = (uint4 *)smem;
-    float *slots = (float *)(smem + (size_t)w.Kc * MR * 256);
+    float *slots = (float *)(smem + (size_t)w.Kc * XR * 256);
 
     const int U = w.Tn * w.Kc;
     int u0, u1;
@@ -481,9 +524,9 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     const int lm = lane & 15, lg = lane >> 4;
     const uint32_t shift = (lane & 1) * 16, keep_lo = (lane & 2) ? 0u : 0xFFFFFFFFu;
 
-    // 1) issue the x loads of the whole chunk (rows >= M read as zero)
+    // 1) issue the x loads of the whole chunk, rows < M only
     const int n8 = w.Kc * 16;
-    const int total = MR * n8;
+    const int total = min(a.M, MR) * n8;
     uint4 v[kStageMax];
     {
         StageWalk sw;
@@ -491,7 +534,7 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
 #pragma unroll
         for (int bb = 0; bb < kStageMax; ++bb) {
             v[bb] = make_uint4(0, 0, 0, 0);
-            if (bb * kThreads + tid < total && sw.m < a.M)
+            if (bb * kThreads + tid < total)
                 v[bb] = *(const uint4 *)(a.x + (size_t)sw.m * a.K + (size_t)(w.g0 + (sw.q8 >> 4)) * kGroup +
                                          (sw.q8 & 15) * 8);
             sw.next(n8);
@@ -501,7 +544,7 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     //    for x below does not wait for them).  A wave with an empty range
     //    re-reads one block, which is harmless.
     BlockWalk pw;                       // prefetch position
-    pw.start(w, a.Nt, min(u0, U - 1));
+    pw.start(w, a.Kb, min(u0, U - 1));
     int up = u0;                        // block index pw points at
     uint4 cb[kDepth];
     uint32_t sb[kDepth];
@@ -509,7 +552,7 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     for (int d = 0; d < kDepth; ++d) {
         cb[d] = load_block(a.codes, pw.b * 64 + lane);
         sb[d] = load_sz<SYM>(a.sz, pw.b * kTileN + lm);
-        if (up + 1 < u1) { pw.next(w, a.Nt); ++up; }
+        if (up + 1 < u1) { pw.next(w, a.Kb); ++up; }
     }
     // 3) write x to LDS in fragment order
     {
@@ -519,19 +562,29 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
         for (int bb = 0; bb < kStageMax; ++bb) {
             if (bb * kThreads + tid < total) {
                 const int c = sw.q8 & 15;          // (kbl, c) with kbl = q8 >> 4
-                xs[sw.q8 * MR + (sw.m & ~15) + ((sw.m & 15) ^ c)] = v[bb];
+                xs[sw.q8 * XR + (sw.m & ~msk) + ((sw.m ^ c) & msk)] = v[bb];
             }
             sw.next(n8);
         }
     }
     lds_barrier();
 
+    // LDS row read by lane row lm of m-tile mt: rows >= M (never staged) read
+    // row M - 1; they only feed output columns >= M, which are not written
+    int xoff[MT][4];           // (row & ~msk) + ((row ^ c) & msk) for c = 4j + lg
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const int r = min(16 * mt + lm, a.M - 1);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) xoff[mt][j] = (r & ~msk) + ((r ^ (4 * j + lg)) & msk);
+    }
+
     if (u0 < u1) {
         v4f acc[MT];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[mt] = v4f{0, 0, 0, 0};
         BlockWalk cw;                   // consume position
-        cw.start(w, a.Nt, u0);
+        cw.start(w, a.Kb, u0);
 
         auto consume = [&](int u, const uint4 &cq, uint32_t szw) {
             v8bf xf[MT][4];
@@ -539,7 +592,7 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
             for (int j = 0; j < 4; ++j)
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
-                    xf[mt][j] = __builtin_bit_cast(v8bf, xs[(cw.kbl * 16 + 4 * j + lg) * MR + 16 * mt + (lm ^ (4 * j + lg))]);
+                    xf[mt][j] = __builtin_bit_cast(v8bf, xs[(cw.kbl * 16 + 4 * j + lg) * XR + xoff[mt][j]]);
             const MfmaDeq d = mfma_setup(szw, shift, keep_lo);
             const uint32_t P[4] = {cq.x, cq.y, cq.z, cq.w};
 #pragma unroll
@@ -557,7 +610,7 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
                     acc[mt] = v4f{0, 0, 0, 0};
                 }
             }
-            cw.next(w, a.Nt);
+            cw.next(w, a.Kb);
         };
 
         int u = u0;
@@ -567,7 +620,7 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
                 consume(u + d, cb[d], sb[d]);
                 cb[d] = load_block(a.codes, pw.b * 64 + lane);
                 sb[d] = load_sz<SYM>(a.sz, pw.b * kTileN + lm);
-                if (up + 1 < u1) { pw.next(w, a.Nt); ++up; }
+                if (up + 1 < u1) { pw.next(w, a.Kb); ++up; }
             }
         }
 #pragma unroll
@@ -586,7 +639,7 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
 // groups and loads the x it needs straight into registers: no x staging in
 // LDS and no barrier before the main loop.  Per group a wave loads every one
 // of its tiles' blocks (contiguous KiB in the device layout) plus that
-// group's x, one group ahead of the compute (two register sets, A and B).
+// group's x, one group ahead of the compute (group_ring with two buffers).
 // Each wave keeps one accumulator per tile; at the end it writes them to its
 // LDS slots and write_out_waves() adds the waves' slots in wave order.
 //
@@ -597,6 +650,7 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
 // Sum over the waves' slots (fixed order) and write y, or fp32 partials plus
 // the last-arrival reduction when the K range is cut (S > 1).  Slot (wave, tl)
 // holds rows x 16 fp32 (row-major, 16 columns).
+template <int TN>
 __device__ inline void write_out_waves(const FwdArgs &a, const WgWork &w, const float *slots, int rows) {
     const int tid = threadIdx.x;
     const int items = w.Tn * a.M * 2;              // half rows of 8 columns
@@ -607,7 +661,7 @@ __device__ inline void write_out_waves(const FwdArgs &a, const WgWork &w, const 
         const int m = rem >> 1, hh = rem & 1;
         float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
         for (int i = 0; i < kWaves; ++i) {
-            const float4 *src = (const float4 *)(slots + (((size_t)i * kTnMax + tl) * rows + m) * 16 + 8 * hh);
+            const float4 *src = (const float4 *)(slots + (((size_t)i * TN + tl) * rows + m) * 16 + 8 * hh);
             const float4 v0 = src[0], v1 = src[1];
             s[0] += v0.x; s[1] += v0.y; s[2] += v0.z; s[3] += v0.w;
             s[4] += v1.x; s[5] += v1.y; s[6] += v1.z; s[7] += v1.w;
@@ -621,12 +675,40 @@ __device__ inline void write_out_waves(const FwdArgs &a, const WgWork &w, const 
             o.w = cvt_pk_bf16(s[6], s[7]);
             *(uint4 *)(a.y + (size_t)m * a.N + n) = o;
         } else {
-            float4 *dst = (float4 *)(a.ws + ((size_t)w.c * a.M + m) * a.N + n);
-            dst[0] = make_float4(s[0], s[1], s[2], s[3]);
-            dst[1] = make_float4(s[4], s[5], s[6], s[7]);
+            store_partial8(a, w, it, s);
         }
     }
     if (!direct) reduce_chunks(a, w);
+}
+
+// Group buffers in flight per wave.  Deeper rings were measured slower for
+// narrow column ranges: every group also reloads its x fragments (4 KiB per
+// wave), so the vector-memory return path of the CU, not HBM latency, is
+// what a deeper ring fills.
+template <int TN>
+constexpr int ring_groups() { return 2; }
+
+// Runs groups [kg0, kg1] through a ring of NG group buffers.  Each buffer is
+// refilled NG groups ahead right after its group is consumed.  The loads are
+// unconditional (a group index past the end is clamped to the last group):
+// a load on only some paths would leave the compiler unsure how many loads
+// are younger than the one it waits for, and it would then drain every load
+// in flight.  The clamped reloads of the last round are not computed.
+template <int NG, typename Buf, typename Load, typename Compute>
+__device__ inline void group_ring(int kg0, int kg1, Buf (&buf)[NG], Load load, Compute compute) {
+#pragma unroll
+    for (int i = 0; i < NG; ++i) load(buf[i], min(kg0 + i, kg1));
+    int kb = kg0;
+    for (; kb + NG <= kg1; kb += NG) {
+#pragma unroll
+        for (int i = 0; i < NG; ++i) {
+            compute(buf[i], kb + i);
+            load(buf[i], min(kb + i + NG, kg1));
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < NG; ++i)
+        if (kb + i <= kg1) compute(buf[i], kb + i);
 }
 
 // The wave's groups [kg0, kg1] and, in the first and last of them, the tile
@@ -643,10 +725,10 @@ struct WaveGroups {
     __device__ inline int tb(int kbl, int Tn) const { return kbl == kg1 ? tb1 : Tn; }
 };
 
-template <bool SYM>
+template <int TN>
 struct MfmaGroup {
-    uint4 c[kTnMax];
-    uint32_t s[kTnMax];
+    uint4 c[TN];
+    uint32_t s[TN];
     v8bf x[4];
 };
 
@@ -659,10 +741,10 @@ __device__ inline v8bf load_xfrag(const FwdArgs &a, int kb, int j, int lane) {
                                                       8 * (lane >> 4)));
 }
 
-template <bool SYM>
+template <int TN, bool SYM>
 __global__ void __launch_bounds__(kThreads) k_mfma16(FwdArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
-    float *slots = (float *)smem;                  // [kWaves][kTnMax][16][16]
+    float *slots = (float *)smem;                  // [kWaves][TN][16][16]
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const ExtractConsts kx;
@@ -673,29 +755,29 @@ __global__ void __launch_bounds__(kThreads) k_mfma16(FwdArgs a) {
     const int lm = lane & 15, lg = lane >> 4;
     const uint32_t shift = (lane & 1) * 16, keep_lo = (lane & 2) ? 0u : 0xFFFFFFFFu;
 
-    v4f acc[kTnMax];
+    v4f acc[TN];
 #pragma unroll
-    for (int t = 0; t < kTnMax; ++t) acc[t] = v4f{0, 0, 0, 0};
+    for (int t = 0; t < TN; ++t) acc[t] = v4f{0, 0, 0, 0};
 
     if (u0 < u1) {
         WaveGroups wg;
         wg.init(u0, u1, Tn);
-        auto load_group = [&](MfmaGroup<SYM> &B, int kbl) {
+        auto load_group = [&](MfmaGroup<TN> &B, int kbl) {
             const int ta = wg.ta(kbl), tb = wg.tb(kbl, Tn);
-            const size_t base = (size_t)(w.g0 + kbl) * a.Nt + w.t0;
+            const size_t base = (size_t)w.t0 * a.Kb + w.g0 + kbl;
 #pragma unroll
-            for (int t = 0; t < kTnMax; ++t) {
-                const size_t b = base + min(max(t, ta), tb - 1);
+            for (int t = 0; t < TN; ++t) {
+                const size_t b = base + (size_t)min(max(t, ta), tb - 1) * a.Kb;
                 B.c[t] = load_block(a.codes, b * 64 + lane);
                 B.s[t] = load_sz<SYM>(a.sz, b * kTileN + lm);
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) B.x[j] = load_xfrag(a, w.g0 + kbl, j, lane);
         };
-        auto compute_group = [&](const MfmaGroup<SYM> &B, int kbl) {
+        auto compute_group = [&](const MfmaGroup<TN> &B, int kbl) {
             const int ta = wg.ta(kbl), tb = wg.tb(kbl, Tn);
 #pragma unroll
-            for (int t = 0; t < kTnMax; ++t) {
+            for (int t = 0; t < TN; ++t) {
                 if (t >= ta && t < tb) {
                     const MfmaDeq d = mfma_setup(B.s[t], shift, keep_lo);
                     const uint32_t P[4] = {B.c[t].x, B.c[t].y, B.c[t].z, B.c[t].w};
@@ -706,25 +788,15 @@ __global__ void __launch_bounds__(kThreads) k_mfma16(FwdArgs a) {
                 }
             }
         };
-        // The next group's loads are issued unconditionally (the last group
-        // is re-read at the end, from cache): a conditional load would
-        // leave the compiler unsure how many loads are younger than the ones
-        // it waits for, and it would then drain every load in flight.
-        MfmaGroup<SYM> A, B;
-        load_group(A, wg.kg0);
-        for (int kbl = wg.kg0; kbl <= wg.kg1; kbl += 2) {
-            load_group(B, min(kbl + 1, wg.kg1));
-            compute_group(A, kbl);
-            load_group(A, min(kbl + 2, wg.kg1));
-            if (kbl + 1 <= wg.kg1) compute_group(B, kbl + 1);
-        }
+        MfmaGroup<TN> ring[ring_groups<TN>()];
+        group_ring(wg.kg0, wg.kg1, ring, load_group, compute_group);
     }
     // D of the 16x16 op: lane l holds rows n = 4(l >> 4) + v of column m = l & 15
 #pragma unroll
-    for (int t = 0; t < kTnMax; ++t)
-        if (t < Tn) *(v4f *)(slots + (((size_t)wave * kTnMax + t) * 16 + lm) * 16 + 4 * lg) = acc[t];
+    for (int t = 0; t < TN; ++t)
+        if (t < Tn) *(v4f *)(slots + (((size_t)wave * TN + t) * 16 + lm) * 16 + 4 * lg) = acc[t];
     lds_barrier();
-    write_out_waves(a, w, slots, 16);
+    write_out_waves<TN>(a, w, slots, 16);
 }
 
 // ---- GEMV: vector-ALU dequantization + v_dot2_f32_bf16 (M <= 4) ---------
@@ -732,17 +804,17 @@ __global__ void __launch_bounds__(kThreads) k_mfma16(FwdArgs a) {
 // Same walk as k_mfma16.  Lane l (b2 = (l >> 2) & 3, g = l >> 4, i = l & 3)
 // holds, for every row m and step j, the bf16 pair (x[m][k], x[m][k + 4]) with
 // k = 128 kb + 32 j + 8 g + i, matching valu_dequant()'s weight pairs.
-template <int MV, bool SYM>
+template <int MV, int TN>
 struct GemvGroup {
-    uint4 c[kTnMaxGemv];
-    uint4 s[kTnMaxGemv];
+    uint4 c[TN];
+    uint4 s[TN];
     uint32_t x[MV][4];
 };
 
-template <int MV, bool SYM>
+template <int MV, int TN, bool SYM>
 __global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
-    float *slots = (float *)smem;                  // [kWaves][kTnMax][MV][16]
+    float *slots = (float *)smem;                  // [kWaves][TN][MV][16]
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const ExtractConsts kx;
@@ -753,9 +825,9 @@ __global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
     const int b2 = (lane >> 2) & 3, li = lane & 3, lg = lane >> 4;
     const uint32_t xsel = (li & 1) ? 0x07060302u : 0x05040100u;   // high or low halves
 
-    float acc[kTnMaxGemv][MV][4];
+    float acc[TN][MV][4];
 #pragma unroll
-    for (int t = 0; t < kTnMaxGemv; ++t)
+    for (int t = 0; t < TN; ++t)
 #pragma unroll
         for (int m = 0; m < MV; ++m)
 #pragma unroll
@@ -764,12 +836,12 @@ __global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
     if (u0 < u1) {
         WaveGroups wg;
         wg.init(u0, u1, Tn);
-        auto load_group = [&](GemvGroup<MV, SYM> &B, int kbl) {
+        auto load_group = [&](GemvGroup<MV, TN> &B, int kbl) {
             const int ta = wg.ta(kbl), tb = wg.tb(kbl, Tn);
-            const size_t base = (size_t)(w.g0 + kbl) * a.Nt + w.t0;
+            const size_t base = (size_t)w.t0 * a.Kb + w.g0 + kbl;
 #pragma unroll
-            for (int t = 0; t < kTnMaxGemv; ++t) {
-                const size_t b = base + min(max(t, ta), tb - 1);
+            for (int t = 0; t < TN; ++t) {
+                const size_t b = base + (size_t)min(max(t, ta), tb - 1) * a.Kb;
                 B.c[t] = load_block(a.codes, b * 64 + lane);
                 if constexpr (SYM) {
                     const uint2 h = *(const uint2 *)((const uint16_t *)a.sz + b * kTileN + 4 * b2);
@@ -789,10 +861,10 @@ __global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
                     B.x[m][j] = __builtin_amdgcn_perm(hi, lo, xsel);
                 }
         };
-        auto compute_group = [&](const GemvGroup<MV, SYM> &B, int kbl) {
+        auto compute_group = [&](const GemvGroup<MV, TN> &B, int kbl) {
             const int ta = wg.ta(kbl), tb = wg.tb(kbl, Tn);
 #pragma unroll
-            for (int t = 0; t < kTnMaxGemv; ++t) {
+            for (int t = 0; t < TN; ++t) {
                 if (t >= ta && t < tb) {
                     const uint32_t s4[4] = {B.s[t].x, B.s[t].y, B.s[t].z, B.s[t].w};
                     const ValuDeq d = valu_setup(s4);
@@ -809,18 +881,12 @@ __global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
                 }
             }
         };
-        GemvGroup<MV, SYM> A, B;          // unconditional next-group loads, see k_mfma16
-        load_group(A, wg.kg0);
-        for (int kbl = wg.kg0; kbl <= wg.kg1; kbl += 2) {
-            load_group(B, min(kbl + 1, wg.kg1));
-            compute_group(A, kbl);
-            load_group(A, min(kbl + 2, wg.kg1));
-            if (kbl + 1 <= wg.kg1) compute_group(B, kbl + 1);
-        }
+        GemvGroup<MV, TN> ring[ring_groups<TN>()];
+        group_ring(wg.kg0, wg.kg1, ring, load_group, compute_group);
     }
     // sum over the 16 lanes sharing b2 (lane bits 0, 1, 4, 5), then one lane per b2 writes
 #pragma unroll
-    for (int t = 0; t < kTnMaxGemv; ++t) {
+    for (int t = 0; t < TN; ++t) {
         if (t < Tn) {
 #pragma unroll
             for (int m = 0; m < MV; ++m) {
@@ -835,13 +901,13 @@ __global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
                     t4[r] = v;
                 }
                 if ((lane & 0x33) == 0)
-                    *(float4 *)(slots + (((size_t)wave * kTnMax + t) * MV + m) * 16 + 4 * b2) =
+                    *(float4 *)(slots + (((size_t)wave * TN + t) * MV + m) * 16 + 4 * b2) =
                         make_float4(t4[0], t4[1], t4[2], t4[3]);
             }
         }
     }
     lds_barrier();
-    write_out_waves(a, w, slots, MV);
+    write_out_waves<TN>(a, w, slots, MV);
 }
 
 // ------------------------------------------------------------------ measurement
@@ -915,60 +981,75 @@ hipError_t launch_dequant(int routine, const uint4 *codes, const void *sz, bool 
 
 typedef void (*FwdKernel)(FwdArgs);
 
-template <bool SYM>
-static FwdKernel pick(int kern, int mrows) {
-    switch (kern) {
-        case kKernMfma16:
-            return k_mfma16<SYM>;
-        case kKernGemv:
-            switch (mrows) {
-                case 1: return k_gemv4<1, SYM>;
-                case 2: return k_gemv4<2, SYM>;
-                case 3: return k_gemv4<3, SYM>;
-                case 4: return k_gemv4<4, SYM>;
-            }
-            break;
-        case kKernStaged:
-            switch (mrows) {
-                case 16: return k_skinny<1, SYM>;
-                case 32: return k_skinny<2, SYM>;
-                case 48: return k_skinny<3, SYM>;
-                case 64: return k_skinny<4, SYM>;
-            }
-            break;
+template <int TN, bool SYM>
+static FwdKernel pick_regs(int kern, int mrows) {
+    if (kern == kKernMfma16) return k_mfma16<TN, SYM>;
+    if constexpr (TN <= kTnMaxGemv) {
+        switch (mrows) {
+            case 1: return k_gemv4<1, TN, SYM>;
+            case 2: return k_gemv4<2, TN, SYM>;
+            case 3: return k_gemv4<3, TN, SYM>;
+            case 4: return k_gemv4<4, TN, SYM>;
+        }
     }
     return nullptr;
 }
 
-static FwdKernel pick_kernel(int kern, int mrows, bool symmetric) {
-    return symmetric ? pick<true>(kern, mrows) : pick<false>(kern, mrows);
+template <bool SYM>
+static FwdKernel pick(int kern, int mrows, int tn) {
+    if (kern == kKernStaged) {
+        switch (mrows) {
+            case 16: return k_skinny<1, SYM>;
+            case 32: return k_skinny<2, SYM>;
+            case 48: return k_skinny<3, SYM>;
+            case 64: return k_skinny<4, SYM>;
+        }
+        return nullptr;
+    }
+    switch (tn) {
+        case 1: return pick_regs<1, SYM>(kern, mrows);
+        case 2: return pick_regs<2, SYM>(kern, mrows);
+        case 3: return pick_regs<3, SYM>(kern, mrows);
+        case 4: return pick_regs<4, SYM>(kern, mrows);
+        case 5: return pick_regs<5, SYM>(kern, mrows);
+        case 6: return pick_regs<6, SYM>(kern, mrows);
+        case 7: return pick_regs<7, SYM>(kern, mrows);
+        case 8: return pick_regs<8, SYM>(kern, mrows);
+    }
+    return nullptr;
 }
 
-const char *kernel_name(int kern, int mrows, bool symmetric) {
-    static char buf[64];
-    if (kern == kKernMfma16) snprintf(buf, sizeof buf, "k_mfma16%s", symmetric ? "<sym>" : "");
-    else if (kern == kKernGemv) snprintf(buf, sizeof buf, "k_gemv4<%d%s>", mrows, symmetric ? ",sym" : "");
+static FwdKernel pick_kernel(int kern, int mrows, int tn, bool symmetric) {
+    return symmetric ? pick<true>(kern, mrows, tn) : pick<false>(kern, mrows, tn);
+}
+
+const char *kernel_name(int kern, int mrows, int tn, bool symmetric) {
+    static thread_local char buf[64];
+    if (kern == kKernMfma16) snprintf(buf, sizeof buf, "k_mfma16<%d%s>", tn, symmetric ? ",sym" : "");
+    else if (kern == kKernGemv) snprintf(buf, sizeof buf, "k_gemv4<%d,%d%s>", mrows, tn, symmetric ? ",sym" : "");
     else snprintf(buf, sizeof buf, "k_skinny<%d%s>", mrows / 16, symmetric ? ",sym" : "");
     return buf;
 }
 
 hipError_t prepare_kernels() {
     for (int sym = 0; sym < 2; ++sym) {
-        (void)hipFuncSetAttribute((const void *)pick_kernel(kKernMfma16, 16, sym),
-                                  hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
-        for (int mv = 1; mv <= kMaxGemvM; ++mv)
-            (void)hipFuncSetAttribute((const void *)pick_kernel(kKernGemv, mv, sym),
+        for (int tn = 1; tn <= kTnMax; ++tn) {
+            (void)hipFuncSetAttribute((const void *)pick_kernel(kKernMfma16, 16, tn, sym),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
+            for (int mv = 1; tn <= kTnMaxGemv && mv <= kMaxGemvM; ++mv)
+                (void)hipFuncSetAttribute((const void *)pick_kernel(kKernGemv, mv, tn, sym),
+                                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
+        }
         for (int mr = 16; mr <= 64; mr += 16)
-            (void)hipFuncSetAttribute((const void *)pick_kernel(kKernStaged, mr, sym),
+            (void)hipFuncSetAttribute((const void *)pick_kernel(kKernStaged, mr, 0, sym),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
     }
     return hipSuccess;
 }
 
-hipError_t launch_forward(int kern, int mrows, bool symmetric, int grid, size_t lds,
+hipError_t launch_forward(int kern, int mrows, int tn, bool symmetric, int grid, size_t lds,
                           const FwdArgs &a, hipStream_t st) {
-    FwdKernel k = pick_kernel(kern, mrows, symmetric);
+    FwdKernel k = pick_kernel(kern, mrows, tn, symmetric);
     if (!k) return hipErrorInvalidValue;
     hipLaunchKernelGGL(k, dim3(grid), dim3(kThreads), lds, st, a);
     return hipGetLastError();

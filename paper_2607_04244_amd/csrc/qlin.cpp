@@ -25,8 +25,9 @@ struct qlin_s {
     bool symmetric = false;
     uint4 *codes = nullptr;      // Nt * Kb blocks of 1 KiB
     void *sz = nullptr;          // Nt * Kb * 16 entries (u32 s|z<<16, or u16 s)
-    float *ws = nullptr;         // split-K partials, ws_rows * N floats
-    int ws_rows = 0;             // bound on S * M of any plan
+    float *ws = nullptr;         // split-K partials, ws_floats fp32
+    int ws_rows = 0;             // S * M the workspace covers for any column split
+    size_t ws_floats = 0;        // 2 * ws_rows * N >= S * Gn * TnMax * M * 16 when S * M <= ws_rows
     uint32_t *counters = nullptr;
     int counters_n = 0;
 };
@@ -105,16 +106,17 @@ int check_zeros(const uint16_t *z, size_t n) {
     return QLIN_OK;
 }
 
-// Does a K chunk of Kc groups fit one workgroup (staged x + one column tile)?
-bool chunk_fits(int path, int rows, int Kc) {
-    return x_chunks(rows, Kc) <= kXChunksMax && lds_bytes(path, rows, Kc, 1) <= kLdsMax;
+// Does a K chunk of Kc groups fit one SKINNY workgroup with M rows (staged x
+// + one column tile)?
+bool chunk_fits(int M, int Kc) {
+    return x_chunks(M, Kc) <= kXChunksMax && lds_bytes(M, Kc, 1) <= kLdsMax;
 }
 
-// Smallest number of K chunks whose chunks fit a workgroup.
-int min_split(int path, int rows, int Kb) {
+// Smallest number of K chunks whose chunks fit a SKINNY workgroup.
+int min_split(int M, int Kb) {
     for (int S = 1; S <= Kb; ++S)
-        if (chunk_fits(path, rows, (Kb + S - 1) / S)) return S;
-    return Kb + 1;   // not even one group fits (cannot happen for rows <= 64)
+        if (chunk_fits(M, (Kb + S - 1) / S)) return S;
+    return Kb + 1;   // not even one group fits (cannot happen for M <= 64)
 }
 
 void free_handle(qlin_s *h) {
@@ -147,14 +149,12 @@ qlin_t create_impl(int64_t K, int64_t N, int64_t group, const uint32_t *packed, 
     const size_t code_bytes = (size_t)N * K / 2;
     const size_t sz_bytes = ngroups * (symmetric ? 2 : 4);
     h->counters_n = std::max(h->Nt, 1);
-    // rows of partial sums the smallest feasible K split needs, for every
-    // row count a kernel template can be launched with
+    // rows of partial sums the smallest feasible K split needs, for every M
+    // a SKINNY launch can have (the other kernels need no split)
     h->ws_rows = kWsRowsMin;
-    for (int rows = 1; rows <= kMaxSkinnyM; ++rows) {
-        const bool gemv = rows <= kMaxGemvM;
-        if (!gemv && rows % 16) continue;
-        const int s_min = min_split(gemv ? kGemv : kSkinny, rows, h->Kb);
-        if (s_min > 1) h->ws_rows = std::max(h->ws_rows, s_min * rows);
+    for (int M = 1; M <= kMaxSkinnyM; ++M) {
+        const int s_min = min_split(M, h->Kb);
+        if (s_min > 1) h->ws_rows = std::max(h->ws_rows, s_min * M);
     }
 
     void *canon = nullptr, *sc = nullptr, *zc = nullptr;
@@ -170,7 +170,9 @@ qlin_t create_impl(int64_t K, int64_t N, int64_t group, const uint32_t *packed, 
     };
     if ((e = dev_alloc((void **)&h->codes, code_bytes)) != hipSuccess) return bail("codes", e);
     if ((e = dev_alloc(&h->sz, sz_bytes)) != hipSuccess) return bail("scales", e);
-    if ((e = dev_alloc((void **)&h->ws, (size_t)h->ws_rows * N * 4)) != hipSuccess) return bail("workspace", e);
+    h->ws_floats = 2 * (size_t)h->ws_rows * N;
+    if (h->ws_floats * 4 > 0xFFFFFFF0u) h->ws_floats = 0xFFFFFFF0u / 4;   // buffer descriptor range
+    if ((e = dev_alloc((void **)&h->ws, h->ws_floats * 4)) != hipSuccess) return bail("workspace", e);
     if ((e = dev_alloc((void **)&h->counters, (size_t)h->counters_n * 4)) != hipSuccess) return bail("counters", e);
     if ((e = dev_alloc(&canon, code_bytes)) != hipSuccess) return bail("staging", e);
     if ((e = dev_alloc(&sc, ngroups * 2)) != hipSuccess) return bail("staging", e);
@@ -206,105 +208,111 @@ struct Plan {
     int kern = 0;
     int mrows = 0;     // template row count (GEMV: M; MFMA kernels: 16 * m-tiles)
     int S = 1, Gn = 1, grid = 1;
+    int tn = 0;        // tile slots of the register-resident kernels: max tiles per range
     size_t lds = 0;
 };
 
-// Auto M-dispatch: vector-ALU GEMV up to this M, matrix cores above.
+// Auto M-dispatch uses the vector-ALU GEMV kernel up to this M (default 0:
+// the matrix-core kernels were measured faster even at M = 1; the GEMV path
+// stays available as an explicit choice).
 int gemv_max_auto() {
     static int v = [] {
         const char *e = getenv("QLIN_GEMV_MAX_M");
-        return e ? std::max(0, std::min(kMaxGemvM, atoi(e))) : 2;
+        return e ? std::max(0, std::min(kMaxGemvM, atoi(e))) : 0;
     }();
     return v;
 }
 
-// M <= 16: register-resident group-major kernel (QLIN_KERN16=regs) or the
-// LDS-staged tile-major kernel (default).
-bool use_regs16() {
-    static bool v = [] {
-        const char *e = getenv("QLIN_KERN16");
-        return e && strcmp(e, "regs") == 0;
-    }();
-    return v;
-}
-
-// Cost (ns) of a (S, Gn) split: the slowest workgroup's share of HBM time,
-// plus the partial-sum traffic and arrival fix-up when the K range is cut.
-double plan_cost(const qlin_s *h, int M, int S, int Gn) {
-    const double bw = 6.0e3;                          // bytes per ns, sustained HBM read
-    const double per_cu = bw / h->num_cu;
+// Estimated time (ns) of one launch, fitted to measurements on MI355X:
+// a fixed part (launch, first HBM round trip, the staged kernel's x
+// staging barrier), the blocks of the busiest workgroup, the staged x
+// chunk, and a fixed cost for the cross-workgroup reduction when the K
+// range is cut.  The register-resident kernel reloads x per group and
+// wave, which costs more per block as M grows.
+double plan_cost(const qlin_s *h, int kern, int M, int S, int Gn) {
     const int Kc = (h->Kb + S - 1) / S, Tn = (h->Nt + Gn - 1) / Gn;
-    const int G = S * Gn;
-    const int rounds = (G + h->num_cu - 1) / h->num_cu;
+    const int rounds = (S * Gn + h->num_cu - 1) / h->num_cu;
+    const double blocks = (double)rounds * Tn * Kc;
+    double t;
+    if (kern == kKernStaged) {
+        const double x_kib = (double)M * Kc * 256.0 / 1024.0;
+        t = 4200.0 + 60.0 * blocks + 12.0 * rounds * x_kib;
+    } else {
+        t = 3300.0 + (60.0 + 3.5 * M) * blocks;
+    }
+    // never faster than streaming the weights at 6 TB/s
     const double blk = 1024.0 + (h->symmetric ? 32.0 : 64.0);
-    const double wg_bytes = (double)Tn * Kc * blk;
-    double t = std::max(rounds * wg_bytes / per_cu, (double)h->Nt * h->Kb * blk / bw);
-    if (S > 1) t += 2.0 * S * M * (double)h->N * 4.0 / bw + 3000.0;
+    t = std::max(t, (double)h->Nt * h->Kb * blk / 6.0e3);
+    if (S > 1) t += 2500.0 + 100.0 * S;
     return t;
 }
 
 int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
+    const bool auto_pick = path == kAuto;
     if (path == kAuto) path = (M <= gemv_max_auto()) ? kGemv : kSkinny;
     if (path == kTiled) path = kSkinny;   // prefill-sized M is run in 64-row slices for now
-    if (path != kGemv && path != kSkinny) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
+    if (path != kGemv && path != kSkinny && path != kRegs) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
     if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= %d", kMaxGemvM);
+    if (path == kRegs && M > 16) return fail(QLIN_ERR_UNSUPPORTED, "REGS path needs M <= 16");
     if (split_k < 0 || split_k > h->Kb) return fail(QLIN_ERR_INVALID, "split_k must be in [0, K/128]");
     const int Mi = (int)std::min<int64_t>(M, kMaxSkinnyM);
     p->path = path;
-    int tn_max;
-    if (path == kGemv) {
-        p->kern = kKernGemv;
-        p->mrows = Mi;
-        tn_max = kTnMaxGemv;
-    } else if (Mi <= 16 && use_regs16()) {
-        p->kern = kKernMfma16;
-        p->mrows = 16;
-        tn_max = kTnMax;
-    } else {
-        p->kern = kKernStaged;
-        p->mrows = 16 * ((Mi + 15) / 16);
-        tn_max = h->Nt;
-    }
-    const bool regs = p->kern != kKernStaged;
-    const int rows = p->mrows;
-    const int gn_min = (h->Nt + tn_max - 1) / tn_max;
+    // candidate kernel families: the forced one, or for the automatic choice
+    // (path SKINNY reached from AUTO) both matrix-core kernels when M <= 16
+    int kerns[2], nk = 0;
+    if (path == kGemv) kerns[nk++] = kKernGemv;
+    else if (path == kRegs) kerns[nk++] = kKernMfma16;
+    else if (auto_pick && Mi <= 16) { kerns[nk++] = kKernMfma16; kerns[nk++] = kKernStaged; }
+    else kerns[nk++] = kKernStaged;
 
-    auto fits = [&](int S, int Gn) {
+    auto tn_max_of = [&](int kern) {
+        return kern == kKernGemv ? kTnMaxGemv : kern == kKernMfma16 ? kTnMax : h->Nt;
+    };
+    auto rows_of = [&](int kern) { return kern == kKernGemv ? Mi : 16 * ((Mi + 15) / 16); };
+    auto fits = [&](int kern, int S, int Gn) {
         const int Kc = (h->Kb + S - 1) / S, Tn = (h->Nt + Gn - 1) / Gn;
-        if (S > 1 && S * Mi > h->ws_rows) return false;
-        if (Gn > h->counters_n || Tn > tn_max) return false;
-        if (regs) return lds_bytes_regs(rows) <= kLdsMax;
-        if (!chunk_fits(kSkinny, rows, Kc)) return false;
-        return lds_bytes(kSkinny, rows, Kc, Tn) <= kLdsMax;
+        if (S > 1 && (size_t)S * Gn * Tn * Mi * 16 > h->ws_floats) return false;
+        if (Gn > h->counters_n || Tn > tn_max_of(kern)) return false;
+        if (kern != kKernStaged) return lds_bytes_regs(rows_of(kern), Tn) <= kLdsMax;
+        if (!chunk_fits(Mi, Kc)) return false;
+        return lds_bytes(Mi, Kc, Tn) <= kLdsMax;
     };
-    auto gn_for = [&](int S) {
-        return std::max(gn_min, std::min(h->Nt, (int)std::lround((double)h->num_cu / S)));
+    // column ranges for S chunks: about one workgroup per CU, but no range
+    // wider than the kernel's tile limit (and more ranges if LDS demands)
+    auto gn_for = [&](int kern, int S) {
+        const int tm = tn_max_of(kern);
+        int Gn = std::max((h->Nt + tm - 1) / tm, std::min(h->Nt, (int)std::lround((double)h->num_cu / S)));
+        Gn = std::min(Gn, h->Nt);
+        while (Gn < h->Nt && !fits(kern, S, Gn)) ++Gn;
+        return Gn;
     };
 
-    int bestS = -1, bestGn = 1;
-    if (split_k > 0) {
-        const int S = (int)split_k;
-        int Gn = std::min(gn_for(S), h->Nt);
-        while (Gn < h->Nt && !fits(S, Gn)) ++Gn;
-        if (!fits(S, Gn)) return fail(QLIN_ERR_UNSUPPORTED, "split_k=%d does not fit (LDS or workspace)", S);
-        bestS = S;
-        bestGn = Gn;
-    } else {
-        double best = 1e300;
-        for (int S = 1; S <= std::min(h->Kb, 64); ++S) {
-            int Gn = std::min(gn_for(S), h->Nt);
-            while (Gn < h->Nt && !fits(S, Gn)) ++Gn;
-            if (!fits(S, Gn)) continue;
-            const double c = plan_cost(h, Mi, S, Gn);
-            if (c < best) { best = c; bestS = S; bestGn = Gn; }
+    int bestK = -1, bestS = -1, bestGn = 1;
+    double best = 1e300;
+    for (int ki = 0; ki < nk; ++ki) {
+        const int kern = kerns[ki];
+        const int s_lo = split_k > 0 ? (int)split_k : 1;
+        const int s_hi = split_k > 0 ? (int)split_k : std::min(h->Kb, 64);
+        for (int S = s_lo; S <= s_hi; ++S) {
+            const int Gn = gn_for(kern, S);
+            if (!fits(kern, S, Gn)) continue;
+            const double c = plan_cost(h, kern, Mi, S, Gn);
+            if (c < best) { best = c; bestK = kern; bestS = S; bestGn = Gn; }
         }
-        if (bestS < 0) return fail(QLIN_ERR_UNSUPPORTED, "no work split fits this shape");
     }
+    if (bestS < 0) {
+        if (split_k > 0) return fail(QLIN_ERR_UNSUPPORTED, "split_k=%d does not fit (LDS or workspace)", (int)split_k);
+        return fail(QLIN_ERR_UNSUPPORTED, "no work split fits this shape");
+    }
+    p->kern = bestK;
+    p->mrows = rows_of(bestK);
     p->S = bestS;
     p->Gn = bestGn;
     p->grid = bestS * bestGn;
+    const bool regs = bestK != kKernStaged;
     const int Kc = (h->Kb + bestS - 1) / bestS, Tn = (h->Nt + bestGn - 1) / bestGn;
-    const size_t need = regs ? lds_bytes_regs(rows) : lds_bytes(kSkinny, rows, Kc, Tn);
+    p->tn = regs ? Tn : 0;
+    const size_t need = regs ? lds_bytes_regs(p->mrows, Tn) : lds_bytes(Mi, Kc, Tn);
     // at least 80 KiB + 1 of LDS per workgroup keeps one workgroup per CU, so
     // the grid spreads over all CUs
     p->lds = std::max(need, (size_t)80 * 1024 + 256);
@@ -329,8 +337,9 @@ int run_forward(qlin_s *h, int path, int64_t split_k, int64_t M, const uint16_t 
     int rc = check_forward_args(h, M, x, y);
     if (rc != QLIN_OK || M == 0) return rc;
     if (path == kSkinny && M > kMaxSkinnyM) return fail(QLIN_ERR_UNSUPPORTED, "SKINNY path needs M <= 64");
+    if (path == kRegs && M > 16) return fail(QLIN_ERR_UNSUPPORTED, "REGS path needs M <= 16");
     if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= %d", kMaxGemvM);
-    if (path < kAuto || path > kTiled) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
+    if (path < kAuto || path > kRegs) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
     int dev = -1;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -360,7 +369,9 @@ int run_forward(qlin_s *h, int path, int64_t split_k, int64_t M, const uint16_t 
         a.Nr = h->Nt % p.Gn;
         a.Kq = h->Kb / p.S;
         a.Kr = h->Kb % p.S;
-        e = launch_forward(p.kern, p.mrows, h->symmetric, p.grid, p.lds, a, st);
+        a.TnMax = a.Nq + (a.Nr > 0 ? 1 : 0);
+        a.ws_bytes = (uint32_t)(h->ws_floats * 4);
+        e = launch_forward(p.kern, p.mrows, p.tn, h->symmetric, p.grid, p.lds, a, st);
         if (e != hipSuccess) return hip_fail(e, "forward launch");
     }
     return QLIN_OK;
@@ -398,15 +409,16 @@ int qlin_plan(qlin_t h, int path, int64_t split_k, int64_t M, char *buf, int64_t
     if (!h) return fail(QLIN_ERR_INVALID, "NULL handle");
     if (!buf || buflen <= 0) return fail(QLIN_ERR_INVALID, "NULL buffer");
     if (M <= 0 || M > kMaxM) return fail(QLIN_ERR_INVALID, "M must be in [1, 65536]");
-    if (path < kAuto || path > kTiled) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
+    if (path < kAuto || path > kRegs) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
     if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= %d", kMaxGemvM);
     if (path == kSkinny && M > kMaxSkinnyM) return fail(QLIN_ERR_UNSUPPORTED, "SKINNY path needs M <= 64");
+    if (path == kRegs && M > 16) return fail(QLIN_ERR_UNSUPPORTED, "REGS path needs M <= 16");
     Plan p;
     int rc = make_plan(h, path, split_k, std::min<int64_t>(M, kMaxSkinnyM), &p);
     if (rc != QLIN_OK) return rc;
     const int64_t slices = (M + kMaxSkinnyM - 1) / kMaxSkinnyM;
     snprintf(buf, (size_t)buflen, "path=%s kernel=%s grid=%d block=%d split=%d ranges=%d lds=%zu launches=%lld",
-             p.path == kGemv ? "gemv" : "skinny", kernel_name(p.kern, p.mrows, h->symmetric), p.grid, kThreads,
+             p.kern == kKernGemv ? "gemv" : p.kern == kKernMfma16 ? "regs" : "skinny", kernel_name(p.kern, p.mrows, p.tn, h->symmetric), p.grid, kThreads,
              p.S, p.Gn, p.lds, (long long)slices);
     return QLIN_OK;
 }

@@ -27,13 +27,13 @@ constexpr int kTnMaxGemv = 4;      // the same for the vector-ALU GEMV kernel
 constexpr size_t kLdsMax = 160 * 1024 - 512;   // dynamic LDS per workgroup (static use is tiny)
 constexpr int kXChunksMax = 8192;  // 16-byte x chunks one workgroup stages (128 KiB)
 
-enum Path { kAuto = 0, kGemv = 1, kSkinny = 2, kTiled = 3 };
+enum Path { kAuto = 0, kGemv = 1, kSkinny = 2, kTiled = 3, kRegs = 4 };
 
 // Kernel families behind the paths (host planning, launch selection).
 enum Kern {
-    kKernGemv = 0,     // k_gemv4: M <= 4, group-major, x in registers
-    kKernMfma16 = 1,   // k_mfma16: M <= 16, group-major, x in registers
-    kKernStaged = 2    // k_skinny<MT>: 16 < M <= 64, x chunk staged in LDS
+    kKernGemv = 0,     // k_gemv4: M <= 4, group-major walk, x in registers (GEMV path)
+    kKernMfma16 = 1,   // k_mfma16: M <= 16, group-major walk, x in registers (REGS path)
+    kKernStaged = 2    // k_skinny<MT>: M <= 64, tile-major walk, x chunk staged in LDS (SKINNY path)
 };
 
 // Arguments of one forward launch.  The K range [0, Kb) of groups is cut into
@@ -46,39 +46,50 @@ struct FwdArgs {
     const void *sz;         // per (tile, group, column): u32 s | z << 16, or u16 s (symmetric)
     const uint16_t *x;      // [M][K] bf16
     uint16_t *y;            // [M][N] bf16
-    float *ws;              // [S][M][N] fp32 partial sums (S > 1)
+    float *ws;              // fp32 partial sums (S > 1): S * Gn regions of TnMax * M * 16
     uint32_t *counters;     // [Gn] arrival counters (S > 1), zero between launches
     int M, K, N, Kb, Nt, S, Gn;
     int Nq, Nr, Kq, Kr;
+    int TnMax;              // Nq + (Nr > 0): tiles of the widest column range
+    uint32_t ws_bytes;      // size of ws (bounds of its buffer descriptor)
 };
 static_assert((kWaves & (kWaves - 1)) == 0, "waves per workgroup must be a power of two");
 
-// x chunks of a K chunk of Kc groups with `rows` staged rows
-inline int x_chunks(int rows, int Kc) { return rows * Kc * 16; }
+// Rows of x a SKINNY workgroup keeps in LDS for M rows (M <= 64): the next
+// power of two >= M up to 16, else whole m-tiles of 16.
+inline int staged_rows(int M) {
+    if (M > 16) return 16 * ((M + 15) / 16);
+    int r = 1;
+    while (r < M) r <<= 1;
+    return r;
+}
 
-// LDS bytes of the register-resident kernels: one slot of rows x 16 fp32
-// per (wave, tile).
-inline size_t lds_bytes_regs(int rows) { return (size_t)kWaves * kTnMax * rows * 16 * 4; }
+// 16-byte x chunks a SKINNY workgroup loads for a K chunk of Kc groups.
+inline int x_chunks(int M, int Kc) { return M * Kc * 16; }
 
-// LDS bytes a forward workgroup needs: the x chunk of Kc groups plus one
-// partial-sum slot (rows x 16 fp32) per (wave, column tile) pair a wave
-// touches; slot = wave + tile is unique, so kWaves + Tn - 1 slots suffice.
-// `rows` = M for GEMV, 16 * m-tiles for SKINNY.
-inline size_t lds_bytes(int path, int rows, int Kc, int Tn) {
-    (void)path;
-    return (size_t)Kc * rows * 256 + (size_t)(kWaves + Tn) * rows * 16 * 4;
+// LDS bytes of the register-resident kernels with tn tile slots: one slot of
+// rows x 16 fp32 per (wave, tile).
+inline size_t lds_bytes_regs(int rows, int tn) { return (size_t)kWaves * tn * rows * 16 * 4; }
+
+// LDS bytes of a SKINNY workgroup with M rows: the x chunk of Kc groups
+// (staged_rows(M) rows) plus one partial-sum slot (16 m-columns per m-tile x
+// 16 fp32) per (wave, column tile) pair a wave touches; slot = wave + tile is
+// unique, so kWaves + Tn - 1 slots suffice.
+inline size_t lds_bytes(int M, int Kc, int Tn) {
+    const int mrows = 16 * ((M + 15) / 16);
+    return (size_t)Kc * staged_rows(M) * 256 + (size_t)(kWaves + Tn) * mrows * 16 * 4;
 }
 
 // Host launchers (kernels.hip).  Each returns the launch status.
 hipError_t launch_repack(const uint32_t *canon, const uint16_t *scales, const uint16_t *zeros,
                          uint4 *codes, void *sz, int K, int N, bool symmetric, hipStream_t st);
-hipError_t launch_forward(int kern, int mrows, bool symmetric, int grid, size_t lds,
+hipError_t launch_forward(int kern, int mrows, int tn, bool symmetric, int grid, size_t lds,
                           const FwdArgs &a, hipStream_t st);
 hipError_t launch_unpack(const uint4 *codes, uint8_t *q, int K, int N, hipStream_t st);
 hipError_t launch_dequant(int routine, const uint4 *codes, const void *sz, bool symmetric,
                           uint16_t *w, int K, int N, hipStream_t st);
 hipError_t prepare_kernels();     // per-process attribute setup (LDS limits)
 hipError_t launch_stream_read(const void *buf, size_t bytes, int grid, uint32_t *sink, hipStream_t st);
-const char *kernel_name(int kern, int mrows, bool symmetric);
+const char *kernel_name(int kern, int mrows, int tn, bool symmetric);
 
 }  // namespace qlin

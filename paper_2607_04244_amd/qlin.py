@@ -21,7 +21,7 @@ QLIN_ERR_ALIGN = -3
 QLIN_ERR_OOM = -4
 QLIN_ERR_HIP = -5
 
-PATH_AUTO, PATH_GEMV, PATH_SKINNY, PATH_TILED = 0, 1, 2, 3
+PATH_AUTO, PATH_GEMV, PATH_SKINNY, PATH_TILED, PATH_REGS = 0, 1, 2, 3, 4
 
 # every symbol include/qlin.h declares
 EXPORTS = ("qlin_create", "qlin_create_symmetric", "qlin_forward", "qlin_forward_path",

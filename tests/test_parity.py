@@ -16,7 +16,7 @@ from synth import gen
 
 pytestmark = pytest.mark.gpu
 
-GEMV, SKINNY, TILED, AUTO = qlin.PATH_GEMV, qlin.PATH_SKINNY, qlin.PATH_TILED, qlin.PATH_AUTO
+GEMV, SKINNY, TILED, AUTO, REGS = qlin.PATH_GEMV, qlin.PATH_SKINNY, qlin.PATH_TILED, qlin.PATH_AUTO, qlin.PATH_REGS
 
 
 def dev(a):
@@ -109,8 +109,10 @@ def _one_hot(M, K, ks):
     return x
 
 
-@pytest.mark.parametrize("path,M,split", [(GEMV, 1, 0), (GEMV, 4, 3), (SKINNY, 16, 0), (SKINNY, 16, 5),
-                                          (SKINNY, 37, 2), (SKINNY, 64, 0), (TILED, 96, 0)])
+@pytest.mark.parametrize("path,M,split", [(GEMV, 1, 0), (GEMV, 4, 3), (SKINNY, 1, 0), (SKINNY, 3, 2),
+                                          (SKINNY, 16, 0), (SKINNY, 16, 5), (SKINNY, 37, 2), (SKINNY, 64, 0),
+                                          (REGS, 1, 0), (REGS, 7, 3), (REGS, 16, 0), (REGS, 16, 4),
+                                          (TILED, 96, 0)])
 def test_one_hot_rows_are_bit_exact(path, M, split):
     K, N = 1280, 320
     c = gen.random_case(31, 1, K, N)
@@ -124,7 +126,7 @@ def test_one_hot_rows_are_bit_exact(path, M, split):
     lin.close()
 
 
-@pytest.mark.parametrize("path", [GEMV, SKINNY])
+@pytest.mark.parametrize("path", [GEMV, SKINNY, REGS])
 def test_codes_equal_zero_point_give_exact_zero(path):
     K, N, M = 768, 96, 4
     rng = np.random.default_rng(2)
@@ -139,7 +141,8 @@ def test_codes_equal_zero_point_give_exact_zero(path):
     lin.close()
 
 
-@pytest.mark.parametrize("path,M", [(GEMV, 2), (GEMV, 3), (SKINNY, 16), (SKINNY, 50)])
+@pytest.mark.parametrize("path,M", [(GEMV, 2), (GEMV, 3), (SKINNY, 1), (SKINNY, 16), (SKINNY, 50),
+                                    (REGS, 1), (REGS, 5), (REGS, 16)])
 def test_integer_case_is_bit_exact(path, M):
     """s = 1, z = 8 (symmetric), x in {-1, 0, 1}: every partial sum is an
     integer below 2^24, so fp32 accumulation is exact in any order."""
@@ -171,7 +174,7 @@ def test_paths_and_splits_match_oracle(K, N, M):
     lin = make(c)
     Kb = K // 128
     splits = sorted({0, 1, min(2, Kb), Kb, max(1, Kb // 3)})
-    paths = [SKINNY, AUTO] + ([GEMV] if M <= 4 else [])
+    paths = [SKINNY, AUTO] + ([GEMV] if M <= 4 else []) + ([REGS] if M <= 16 else [])
     for path in paths:
         for split in splits:
             y = run_split(lin, c["x"], path, split)     # split 0 (the planner's) always runs
@@ -193,7 +196,7 @@ def test_symmetric_forward_matches_oracle():
     c = gen.random_case(77, 16, 2560, 1024)
     lin = make(c, symmetric=True)
     y_ref = oracle(c, symmetric=True)
-    for path, M in ((GEMV, 1), (GEMV, 2), (SKINNY, 16)):
+    for path, M in ((GEMV, 1), (GEMV, 2), (SKINNY, 16), (SKINNY, 3), (REGS, 1), (REGS, 16)):
         assert_close(run(lin, c["x"][:M], path), y_ref[:M], f"path={path}")
     lin.close()
 
@@ -202,7 +205,7 @@ def test_config0_single_linear():
     c = gen.linear_case(0)
     lin = make(c)
     y_ref = oracle(c)
-    for path in (AUTO, GEMV, SKINNY):
+    for path in (AUTO, GEMV, SKINNY, REGS):
         assert_close(run(lin, c["x"], path), y_ref, f"path={path}")
     lin.close()
 
@@ -215,6 +218,7 @@ def test_config1_draft_block_verify_full_size():
     y_ref = oracle(c)
     assert_close(run(lin, c["x"]), y_ref, "auto")
     assert_close(run(lin, c["x"], SKINNY, 2), y_ref, "skinny split 2")
+    assert_close(run(lin, c["x"], REGS), y_ref, "regs")
     lin.close()
 
 
@@ -223,7 +227,7 @@ def test_config2_down_projection_with_outliers(M):
     c = gen.linear_case(2, M=M)
     lin = make(c)
     y_ref = oracle(c)
-    paths = (AUTO, SKINNY, GEMV) if M <= 4 else (AUTO, SKINNY)
+    paths = (AUTO, SKINNY, REGS, GEMV) if M <= 4 else (AUTO, SKINNY, REGS)
     for path in paths:
         assert_close(run(lin, c["x"], path), y_ref, f"M={M} path={path}")
     lin.close()
@@ -250,8 +254,8 @@ def test_zero_rows_is_a_noop_and_repeat_calls_agree():
     # every reduction runs in a fixed order, so repeated calls give identical
     # bits; split-K arrival counters must reset themselves between calls
     y_ref = oracle(c)
-    for path, split in ((SKINNY, 4), (SKINNY, 1), (GEMV, 3)):
-        M = 16 if path == SKINNY else 4
+    for path, split in ((SKINNY, 4), (SKINNY, 1), (GEMV, 3), (REGS, 5), (REGS, 1)):
+        M = 4 if path == GEMV else 16
         first = run(lin, c["x"][:M], path, split)
         assert_close(first, y_ref[:M])
         for _ in range(3):
@@ -286,6 +290,7 @@ def test_forward_argument_errors():
     assert f(lin.h, AUTO, 0, 65537, xp, yp, None) == qlin.QLIN_ERR_UNSUPPORTED
     assert f(lin.h, GEMV, 0, 5, xp, yp, None) == qlin.QLIN_ERR_UNSUPPORTED
     assert f(lin.h, SKINNY, 0, 65, xp, yp, None) == qlin.QLIN_ERR_UNSUPPORTED
+    assert f(lin.h, REGS, 0, 17, xp, yp, None) == qlin.QLIN_ERR_UNSUPPORTED
     assert f(lin.h, 7, 0, 4, xp, yp, None) == qlin.QLIN_ERR_INVALID
     assert f(lin.h, AUTO, 3, 4, xp, yp, None) == qlin.QLIN_ERR_INVALID          # split_k > K/128
     assert f(lin.h, AUTO, -1, 4, xp, yp, None) == qlin.QLIN_ERR_INVALID
