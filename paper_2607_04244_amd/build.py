@@ -11,32 +11,54 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libqlin.so")
-SOURCES = ["kernels.hip", "qlin.cpp"]
+# (source, extra flags).  tiled.hip keeps matrix-core results in VGPRs: its
+# dequantizing 4x4x4 products feed vector instructions directly.
+SOURCES = [("kernels.hip", []), ("tiled.hip", ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]), ("qlin.cpp", [])]
 ARCH = "gfx950"
 
 # Packed-fp32 vector instructions are switched off in the device pass; the
 # host pass warns that it does not know the feature, which is harmless.
 HIP_FLAGS = [
-    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
+    f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-Wall", "-Wno-unused-function",
 ]
+NOISE = "is not a recognized feature for this target"
+
+
+def _errs(r):
+    return "\n".join(l for l in (r.stderr or "").splitlines() if NOISE not in l)
 
 
 def build(verbose=False, extra_flags=()):
+    """Compile every source to an object (in parallel), then link the library."""
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+    inc = ["-I", os.path.join(HERE, "..", "include")]
+    objs, procs = [], []
+    for src, flags in SOURCES:
+        obj = os.path.join(CSRC, os.path.splitext(src)[0] + ".o")
+        cmd = [hipcc, *HIP_FLAGS, *flags, *extra_flags, *inc, "-c", os.path.join(CSRC, src), "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)))
+        objs.append(obj)
+    failed = []
+    for src, p in procs:
+        out, err = p.communicate()
+        r = subprocess.CompletedProcess(p.args, p.returncode, out, err)
+        if r.returncode != 0:
+            failed.append(f"{src}:\n{_errs(r)}")
+        elif verbose and _errs(r).strip():
+            print(_errs(r), file=sys.stderr)
+    if failed:
+        raise RuntimeError("hipcc failed:\n" + "\n".join(failed))
     tmp = LIB + ".tmp"
-    cmd = [hipcc, *HIP_FLAGS, *extra_flags, "-I", os.path.join(HERE, "..", "include"),
-           *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
+    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)
-    noise = "is not a recognized feature for this target"
-    errs = "\n".join(l for l in (r.stderr or "").splitlines() if noise not in l)
     if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed ({r.returncode}):\n{errs}")
-    if verbose and errs.strip():
-        print(errs, file=sys.stderr)
+        raise RuntimeError(f"link failed ({r.returncode}):\n{_errs(r)}")
+    for o in objs:
+        os.remove(o)
     os.replace(tmp, LIB)
     return LIB
 

@@ -30,150 +30,11 @@
 // v_dot2_f32_bf16 on the same extracted pairs.  Both routes are bit-identical
 // to the definition; the unpack/dequantize test hooks check that.
 
-#include "qlin_internal.h"
+#include "device_common.h"
 
 #include <cstdio>
 
 namespace qlin {
-
-typedef short v4s __attribute__((ext_vector_type(4)));
-typedef float v4f __attribute__((ext_vector_type(4)));
-typedef float v2f __attribute__((ext_vector_type(2)));
-typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
-typedef __bf16 v2bf __attribute__((ext_vector_type(2)));
-typedef uint32_t v4u __attribute__((ext_vector_type(4)));
-typedef uint32_t v2u __attribute__((ext_vector_type(2)));
-
-// ------------------------------------------------------------------ layout
-
-// Column (within the tile) and k (within the group) of nibble p of word j of lane l.
-__host__ __device__ inline void block_coord(int l, int j, int p, int &n16, int &k128) {
-    const int r = 2 * (p & 1) + (p >> 2);
-    const int h = (p >> 1) & 1;
-    n16 = 4 * ((l >> 2) & 3) + r;
-    k128 = 32 * j + 8 * (l >> 4) + 4 * h + (l & 3);
-}
-
-// ------------------------------------------------------------------ small helpers
-
-__device__ inline uint32_t cvt_pk_bf16(float lo, float hi) {
-    v2f f = {lo, hi};
-    v2bf b = __builtin_convertvector(f, v2bf);   // round to nearest even
-    return __builtin_bit_cast(uint32_t, b);
-}
-
-__device__ inline uint16_t cvt_bf16(float v) {
-    __bf16 b = (__bf16)v;
-    return __builtin_bit_cast(uint16_t, b);
-}
-
-__device__ inline float bf16_lo_to_f32(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ inline float bf16_hi_to_f32(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
-
-// The four "128 + q" bf16 pairs of one packed word: pair i holds nibbles i
-// (low half) and i + 4 (high half).  Each pair is one v_and_or_b32; the two
-// constants live in registers (gfx9 VOP3 takes no literal), loaded once per
-// kernel by ExtractConsts.
-struct ExtractConsts {
-    uint32_t mask, magic;
-    __device__ inline ExtractConsts() {
-        // opaque to the optimizer, so the values stay in registers
-        mask = __builtin_amdgcn_readfirstlane(0x000F000Fu);
-        magic = 0x43004300u;                        // bf16 128.0 in both halves
-        asm volatile("" : "+v"(magic));
-    }
-};
-struct Pairs { uint32_t a0, a1, a2, a3; };
-__device__ inline Pairs extract_pairs(uint32_t P, const ExtractConsts &k) {
-    Pairs o;
-    o.a0 = (P & k.mask) | k.magic;
-    o.a1 = ((P >> 4) & k.mask) | k.magic;
-    o.a2 = ((P >> 8) & k.mask) | k.magic;
-    o.a3 = ((P >> 12) & k.mask) | k.magic;
-    return o;
-}
-
-// One lane's 16 bytes of a weight block.
-__device__ inline uint4 load_block(const uint4 *codes, size_t idx) { return codes[idx]; }
-
-// s | z << 16 word of a column (symmetric handles store only s; z = 8).
-template <bool SYM>
-__device__ inline uint32_t load_sz(const void *sz, size_t idx) {
-    if constexpr (SYM) {
-        return (uint32_t)((const uint16_t *)sz)[idx] | (0x4100u << 16);
-    } else {
-        return ((const uint32_t *)sz)[idx];
-    }
-}
-
-// --- matrix-core dequantization ------------------------------------------
-
-struct MfmaDeq { v4s bdiag; v4f c4; };
-
-// Per-group constants of lane l for column n = 16 t + (l & 15):
-// B = diag(s) in the 4x4 block layout (this lane supplies B[r][l & 3],
-// non-zero only for r = l & 3) and C = -(128 + z) * s in all four rows.
-__device__ inline MfmaDeq mfma_setup(uint32_t sz, uint32_t shift, uint32_t keep_lo) {
-    const float s = bf16_lo_to_f32(sz);
-    const float z = bf16_hi_to_f32(sz);
-    const float c = -((z + 128.0f) * s);
-    const uint32_t v = (sz & 0xFFFFu) << shift;     // s in half (l & 1)
-    const uint32_t b0 = v & keep_lo, b1 = v & ~keep_lo;
-    MfmaDeq d;
-    d.bdiag = __builtin_bit_cast(v4s, v2u{b0, b1});
-    d.c4 = v4f{c, c, c, c};
-    return d;
-}
-
-// Dequantize one packed word into the 8 bf16 A-operand values of
-// v_mfma_f32_16x16x32_bf16 (row n = l & 15): element e holds
-// w[n][32j + 8(l >> 4) + e].
-__device__ inline v8bf mfma_dequant(uint32_t P, const MfmaDeq &d, const ExtractConsts &k) {
-    const Pairs a = extract_pairs(P, k);
-    const v4s A0 = __builtin_bit_cast(v4s, v2u{a.a0, a.a1});
-    const v4s A1 = __builtin_bit_cast(v4s, v2u{a.a2, a.a3});
-    const v4f d0 = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(A0, d.bdiag, d.c4, 0, 0, 0);
-    const v4f d1 = __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(A1, d.bdiag, d.c4, 0, 0, 0);
-    const v4u w = {cvt_pk_bf16(d0[0], d0[1]), cvt_pk_bf16(d0[2], d0[3]),
-                   cvt_pk_bf16(d1[0], d1[1]), cvt_pk_bf16(d1[2], d1[3])};
-    return __builtin_bit_cast(v8bf, w);
-}
-
-// --- vector-ALU dequantization -------------------------------------------
-
-// Constants for the four columns n = 16 t + 4 * ((l >> 2) & 3) + r of lane l.
-struct ValuDeq { uint32_t sl[4], sh[4]; float c[4]; };
-
-__device__ inline ValuDeq valu_setup(const uint32_t sz[4]) {
-    ValuDeq d;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-        const float s = bf16_lo_to_f32(sz[r]);
-        const float z = bf16_hi_to_f32(sz[r]);
-        d.c[r] = -((z + 128.0f) * s);
-        d.sl[r] = sz[r] & 0xFFFFu;   // bf16 pair (s, 0)
-        d.sh[r] = sz[r] << 16;       // bf16 pair (0, s)
-    }
-    return d;
-}
-
-__device__ inline float dot2(uint32_t a, uint32_t b, float c) {
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(v2bf, a), __builtin_bit_cast(v2bf, b), c, false);
-}
-
-// Dequantize one packed word: pr[r] = bf16 pair (w[n_r][k0], w[n_r][k0 + 4]) with
-// k0 = 32j + 8(l >> 4) + (l & 3).
-__device__ inline void valu_dequant(uint32_t P, const ValuDeq &d, const ExtractConsts &k, uint32_t pr[4]) {
-    const Pairs a = extract_pairs(P, k);
-    const float w00 = dot2(a.a0, d.sl[0], d.c[0]), w01 = dot2(a.a0, d.sh[1], d.c[1]);
-    const float w02 = dot2(a.a1, d.sl[2], d.c[2]), w03 = dot2(a.a1, d.sh[3], d.c[3]);
-    const float w10 = dot2(a.a2, d.sl[0], d.c[0]), w11 = dot2(a.a2, d.sh[1], d.c[1]);
-    const float w12 = dot2(a.a3, d.sl[2], d.c[2]), w13 = dot2(a.a3, d.sh[3], d.c[3]);
-    pr[0] = cvt_pk_bf16(w00, w10);
-    pr[1] = cvt_pk_bf16(w01, w11);
-    pr[2] = cvt_pk_bf16(w02, w12);
-    pr[3] = cvt_pk_bf16(w03, w13);
-}
 
 // ------------------------------------------------------------------ repack
 
@@ -1025,7 +886,8 @@ static FwdKernel pick_kernel(int kern, int mrows, int tn, bool symmetric) {
 
 const char *kernel_name(int kern, int mrows, int tn, bool symmetric) {
     static thread_local char buf[64];
-    if (kern == kKernMfma16) snprintf(buf, sizeof buf, "k_mfma16<%d%s>", tn, symmetric ? ",sym" : "");
+    if (kern == kKernTiled) snprintf(buf, sizeof buf, "k_tiled%s", symmetric ? "<sym>" : "");
+    else if (kern == kKernMfma16) snprintf(buf, sizeof buf, "k_mfma16<%d%s>", tn, symmetric ? ",sym" : "");
     else if (kern == kKernGemv) snprintf(buf, sizeof buf, "k_gemv4<%d,%d%s>", mrows, tn, symmetric ? ",sym" : "");
     else snprintf(buf, sizeof buf, "k_skinny<%d%s>", mrows / 16, symmetric ? ",sym" : "");
     return buf;

@@ -247,10 +247,32 @@ double plan_cost(const qlin_s *h, int kern, int M, int S, int Gn) {
     return t;
 }
 
+// TILED plan: one launch over all M rows, 128 x 256 output blocks, grid
+// padded to a multiple of 8 column blocks (see k_tiled).
+int make_tiled_plan(const qlin_s *h, int64_t split_k, int64_t M, Plan *p) {
+    if (split_k > 1) return fail(QLIN_ERR_UNSUPPORTED, "split_k=%d does not fit (TILED path runs the whole K range)", (int)split_k);
+    if (M * h->K >= ((int64_t)1 << 31)) return fail(QLIN_ERR_UNSUPPORTED, "TILED path needs M * K < 2^31");
+    const int Mt = (int)((M + kTiledBM - 1) / kTiledBM);
+    const int Gn = (h->Nt + 15) / 16;
+    p->path = kTiled;
+    p->kern = kKernTiled;
+    p->mrows = kTiledBM;
+    p->S = 1;
+    p->Gn = Gn;
+    p->tn = 0;
+    p->grid = 8 * ((Gn + 7) / 8) * Mt;
+    p->lds = 0;
+    return QLIN_OK;
+}
+
+// Rows from which qlin_forward uses the TILED kernel instead of 64-row
+// slices of the decode kernels.
+constexpr int64_t kTiledFromM = kMaxSkinnyM + 1;
+
 int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
     const bool auto_pick = path == kAuto;
+    if (path == kTiled || (path == kAuto && M >= kTiledFromM)) return make_tiled_plan(h, split_k, M, p);
     if (path == kAuto) path = (M <= gemv_max_auto()) ? kGemv : kSkinny;
-    if (path == kTiled) path = kSkinny;   // prefill-sized M is run in 64-row slices for now
     if (path != kGemv && path != kSkinny && path != kRegs) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
     if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= %d", kMaxGemvM);
     if (path == kRegs && M > 16) return fail(QLIN_ERR_UNSUPPORTED, "REGS path needs M <= 16");
@@ -345,7 +367,27 @@ int run_forward(qlin_s *h, int path, int64_t split_k, int64_t M, const uint16_t 
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
     if (dev != h->device) return fail(QLIN_ERR_INVALID, "handle belongs to device %d, current is %d", h->device, dev);
     hipStream_t st = (hipStream_t)stream;
-    // rows beyond 64 run as consecutive 64-row slices
+    if (path == kTiled || (path == kAuto && M >= kTiledFromM)) {
+        Plan p;
+        rc = make_tiled_plan(h, split_k, M, &p);
+        if (rc != QLIN_OK) return rc;
+        TiledArgs a;
+        a.codes = h->codes;
+        a.sz = h->sz;
+        a.x = x;
+        a.y = y;
+        a.M = (int)M;
+        a.K = (int)h->K;
+        a.N = (int)h->N;
+        a.Kb = h->Kb;
+        a.Nt = h->Nt;
+        a.Mt = (int)((M + kTiledBM - 1) / kTiledBM);
+        a.Gn = p.Gn;
+        e = launch_tiled(h->symmetric, a, p.grid, st);
+        if (e != hipSuccess) return hip_fail(e, "tiled launch");
+        return QLIN_OK;
+    }
+    // GEMV / SKINNY / REGS: rows beyond 64 run as consecutive 64-row slices
     for (int64_t m0 = 0; m0 < M; m0 += kMaxSkinnyM) {
         const int64_t Ms = std::min<int64_t>(kMaxSkinnyM, M - m0);
         Plan p;
@@ -414,12 +456,14 @@ int qlin_plan(qlin_t h, int path, int64_t split_k, int64_t M, char *buf, int64_t
     if (path == kSkinny && M > kMaxSkinnyM) return fail(QLIN_ERR_UNSUPPORTED, "SKINNY path needs M <= 64");
     if (path == kRegs && M > 16) return fail(QLIN_ERR_UNSUPPORTED, "REGS path needs M <= 16");
     Plan p;
-    int rc = make_plan(h, path, split_k, std::min<int64_t>(M, kMaxSkinnyM), &p);
+    const bool tiled = path == kTiled || (path == kAuto && M >= kTiledFromM);
+    int rc = tiled ? make_tiled_plan(h, split_k, M, &p) : make_plan(h, path, split_k, std::min<int64_t>(M, kMaxSkinnyM), &p);
     if (rc != QLIN_OK) return rc;
-    const int64_t slices = (M + kMaxSkinnyM - 1) / kMaxSkinnyM;
+    const int64_t slices = tiled ? 1 : (M + kMaxSkinnyM - 1) / kMaxSkinnyM;
+    static const char *names[] = {"gemv", "regs", "skinny", "tiled"};
     snprintf(buf, (size_t)buflen, "path=%s kernel=%s grid=%d block=%d split=%d ranges=%d lds=%zu launches=%lld",
-             p.kern == kKernGemv ? "gemv" : p.kern == kKernMfma16 ? "regs" : "skinny", kernel_name(p.kern, p.mrows, p.tn, h->symmetric), p.grid, kThreads,
-             p.S, p.Gn, p.lds, (long long)slices);
+             names[p.kern], kernel_name(p.kern, p.mrows, p.tn, h->symmetric), p.grid,
+             tiled ? kTiledWaves * 64 : kThreads, p.S, p.Gn, p.lds, (long long)slices);
     return QLIN_OK;
 }
 

@@ -33,7 +33,8 @@ enum Path { kAuto = 0, kGemv = 1, kSkinny = 2, kTiled = 3, kRegs = 4 };
 enum Kern {
     kKernGemv = 0,     // k_gemv4: M <= 4, group-major walk, x in registers (GEMV path)
     kKernMfma16 = 1,   // k_mfma16: M <= 16, group-major walk, x in registers (REGS path)
-    kKernStaged = 2    // k_skinny<MT>: M <= 64, tile-major walk, x chunk staged in LDS (SKINNY path)
+    kKernStaged = 2,   // k_skinny<MT>: M <= 64, tile-major walk, x chunk staged in LDS (SKINNY path)
+    kKernTiled = 3     // k_tiled: any M, 128 x 256 output blocks, x and weights staged in LDS (TILED path)
 };
 
 // Arguments of one forward launch.  The K range [0, Kb) of groups is cut into
@@ -54,6 +55,25 @@ struct FwdArgs {
     uint32_t ws_bytes;      // size of ws (bounds of its buffer descriptor)
 };
 static_assert((kWaves & (kWaves - 1)) == 0, "waves per workgroup must be a power of two");
+
+// TILED kernel (prefill-sized M): a workgroup of kTiledWaves waves computes
+// kTiledBM rows x kTiledBN columns; each wave owns kTiledNT column tiles.
+constexpr int kTiledWaves = 4;
+constexpr int kTiledNT = 4;
+constexpr int kTiledBM = 128;
+constexpr int kTiledMS = kTiledBM / 16;                    // 16-row m-subtiles
+constexpr int kTiledBN = kTiledWaves * kTiledNT * kTileN;  // 256 columns
+constexpr int kTiledXLoads = kTiledBM * 16 / (kTiledWaves * 64);   // direct-to-LDS loads per wave and group
+
+struct TiledArgs {
+    const uint4 *codes;
+    const void *sz;
+    const uint16_t *x;
+    uint16_t *y;
+    int M, K, N, Kb, Nt;
+    int Mt;                 // row blocks: ceil(M / kTiledBM)
+    int Gn;                 // column blocks: ceil(Nt / 16)
+};
 
 // Rows of x a SKINNY workgroup keeps in LDS for M rows (M <= 64): the next
 // power of two >= M up to 16, else whole m-tiles of 16.
@@ -89,6 +109,7 @@ hipError_t launch_unpack(const uint4 *codes, uint8_t *q, int K, int N, hipStream
 hipError_t launch_dequant(int routine, const uint4 *codes, const void *sz, bool symmetric,
                           uint16_t *w, int K, int N, hipStream_t st);
 hipError_t prepare_kernels();     // per-process attribute setup (LDS limits)
+hipError_t launch_tiled(bool symmetric, const TiledArgs &a, int grid, hipStream_t st);
 hipError_t launch_stream_read(const void *buf, size_t bytes, int grid, uint32_t *sink, hipStream_t st);
 const char *kernel_name(int kern, int mrows, int tn, bool symmetric);
 

@@ -1,0 +1,202 @@
+// Prefill-sized M: the tiled W4A16 GEMM kernel for CDNA4 (gfx950).
+//
+// Same layer as the decode kernels (Sec. 2.1, 3.2, 3.3 of arXiv 2607.04244):
+// each weight is the exact (q - z) * s rounded once to bf16, y = x . w^T in
+// fp32, rounded once to bf16.  This file is compiled on its own with
+// matrix-core results kept in ordinary VGPRs (see build.py): the
+// dequantizing 4x4x4 products feed vector instructions, and with results in
+// accumulation registers every value would need a copy back.
+
+#include "device_common.h"
+
+namespace qlin {
+
+// ---- TILED: prefill-sized M (GEMM), matrix-core dequantization ----------
+//
+// A workgroup of kTiledWaves waves computes a kTiledBM x kTiledBN block of y:
+// rows [128 im, 128 im + 128) and column tiles [16 jn, 16 jn + 16); wave w
+// owns tiles 16 jn + 4 w + t, t < 4, for all 128 rows.  Per group kb the
+// workgroup stages the 128 x 128 x-tile in LDS with direct-to-LDS loads
+// (global_load_lds_dwordx4, no VGPR round trip), double-buffered one group
+// ahead, and each wave loads its four weight blocks one group ahead into
+// registers.  Dequantization (the matrix-core route) produces the A operand
+// of v_mfma_f32_16x16x32_bf16 directly; each x fragment read from LDS feeds
+// the four tiles of the wave.
+//
+// x tile in LDS: 16-byte chunk (row r, c) = x[row][128 kb + 8c .. + 8],
+// c < 16, at slot 16 r + (c ^ (r & 15)): a wave's direct-to-LDS load fills 64
+// consecutive slots (4 rows, each a permutation of one row's 256 bytes, so
+// the global reads stay coalesced), and the operand reads (16 lanes = 16
+// rows of one c) hit 16 distinct bank groups.
+//
+// Workgroups sharing a column block are given block indices that are equal
+// modulo 8 (the XCD a workgroup runs on) and adjacent in dispatch order, so
+// the column block's weights are fetched once into that XCD's L2 and reused
+// by the row blocks.  Rows >= M and tiles >= Nt load a clamped valid row or
+// tile and are not written.
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef __attribute__((address_space(1))) void glb_void_t;
+
+template <bool SYM>
+__global__ void __launch_bounds__(kTiledWaves * 64, 1) k_tiled(TiledArgs a) {
+    __shared__ __align__(16) uint4 xs[2][kTiledBM * 16];
+    // weight blocks of the workgroup's 16 tiles (wave w: tiles 4 w .. 4 w + 3,
+    // 1 KiB each) and their s|z words (64 per tile; lane l of a load writes
+    // the word of column l & 15, the other 48 are copies), double-buffered
+    __shared__ __align__(16) uint4 ws_codes[2][kTiledWaves * kTiledNT * 64];
+    __shared__ __align__(16) uint32_t ws_sz[2][kTiledWaves * kTiledNT * 64];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const ExtractConsts kx;
+    // block index -> (column block jn, row block im)
+    const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3;
+    const int jg = q / a.Mt;                          // once per workgroup
+    const int im = q - jg * a.Mt;
+    const int jn = jg * 8 + xcd;
+    if (jn >= a.Gn) return;                           // uniform: padding of the grid
+    const int lm = lane & 15, lg = lane >> 4;
+    const uint32_t shift = (lane & 1) * 16, keep_lo = (lane & 2) ? 0u : 0xFFFFFFFFu;
+
+    // element offsets (from x, group 0) of this lane's direct-to-LDS loads:
+    // load i of wave w fills rows 32 w + 4 i + (lane >> 4), slot position
+    // lane & 15, which holds chunk (lane & 15) ^ (row & 15) of that row.
+    // The planner keeps M * K below 2^31.
+    uint32_t xo[kTiledXLoads];
+#pragma unroll
+    for (int i = 0; i < kTiledXLoads; ++i) {
+        const int r = wave * (kTiledBM / kTiledWaves) + 4 * i + lg;
+        const int row = min(im * kTiledBM + r, a.M - 1);
+        xo[i] = (uint32_t)row * (uint32_t)a.K + (uint32_t)(((lane & 15) ^ (r & 15)) * 8);
+    }
+    auto load_x = [&](int kb, int buf) {
+#pragma unroll
+        for (int i = 0; i < kTiledXLoads; ++i) {
+            const int r0 = wave * (kTiledBM / kTiledWaves) + 4 * i;
+            __builtin_amdgcn_global_load_lds((glb_void_t *)(a.x + xo[i] + (uint32_t)kb * kGroup),
+                                             (lds_void_t *)&xs[buf][r0 * 16], 16, 0, 0);
+        }
+    };
+    // this wave's four tiles (clamped for loads): uint4 index of block (t, 0)
+    uint32_t wo[kTiledNT];
+#pragma unroll
+    for (int t = 0; t < kTiledNT; ++t)
+        wo[t] = (uint32_t)min(jn * 16 + wave * kTiledNT + t, a.Nt - 1) * (uint32_t)a.Kb;
+    auto load_w = [&](int kb, int buf) {
+#pragma unroll
+        for (int t = 0; t < kTiledNT; ++t) {
+            const uint32_t b = wo[t] + (uint32_t)kb;
+            const int slot = (wave * kTiledNT + t) * 64;
+            __builtin_amdgcn_global_load_lds((glb_void_t *)(a.codes + (size_t)b * 64 + lane),
+                                             (lds_void_t *)&ws_codes[buf][slot], 16, 0, 0);
+            if constexpr (SYM) {
+                // 2-byte scales: one dword per lane covers columns 2i, 2i + 1;
+                // lane l & 7 then picks its half below
+                __builtin_amdgcn_global_load_lds((glb_void_t *)((const uint32_t *)a.sz + (size_t)b * (kTileN / 2) + (lane & 7)),
+                                                 (lds_void_t *)&ws_sz[buf][slot], 4, 0, 0);
+            } else {
+                __builtin_amdgcn_global_load_lds((glb_void_t *)((const uint32_t *)a.sz + (size_t)b * kTileN + lm),
+                                                 (lds_void_t *)&ws_sz[buf][slot], 4, 0, 0);
+            }
+        }
+    };
+    // this lane's code words and s|z word of tile t from LDS
+    auto read_w = [&](int buf, uint4 (&cw)[kTiledNT], uint32_t (&sw)[kTiledNT]) {
+#pragma unroll
+        for (int t = 0; t < kTiledNT; ++t) {
+            const int slot = (wave * kTiledNT + t) * 64;
+            cw[t] = ws_codes[buf][slot + lane];
+            if constexpr (SYM) {
+                const uint32_t pair = ws_sz[buf][slot + (lm >> 1)];
+                sw[t] = ((lm & 1) ? (pair >> 16) : (pair & 0xFFFFu)) | (0x4100u << 16);
+            } else {
+                sw[t] = ws_sz[buf][slot + lm];
+            }
+        }
+    };
+
+    v4f acc[kTiledMS][kTiledNT];
+#pragma unroll
+    for (int ms = 0; ms < kTiledMS; ++ms)
+#pragma unroll
+        for (int t = 0; t < kTiledNT; ++t) acc[ms][t] = v4f{0, 0, 0, 0};
+
+    // LDS slot of this lane's operand read (row 16 ms + lm, chunk 4 j + lg)
+    auto xslot = [&](int ms, int j) { return ms * 256 + lm * 16 + ((4 * j + lg) ^ lm); };
+
+    auto compute = [&](int buf) {
+        uint4 cw[kTiledNT];
+        uint32_t sw[kTiledNT];
+        read_w(buf, cw, sw);
+        MfmaDeq d[kTiledNT];
+#pragma unroll
+        for (int t = 0; t < kTiledNT; ++t) d[t] = mfma_setup(sw[t], shift, keep_lo);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            // one k-step of 32 at a time, and x fragments read one m-subtile
+            // ahead of their products: bounds the live registers so that the
+            // accumulators and operands fit the VGPR file
+            __builtin_amdgcn_sched_barrier(0);
+            v8bf wa[kTiledNT];
+#pragma unroll
+            for (int t = 0; t < kTiledNT; ++t) {
+                const uint32_t P = j == 0 ? cw[t].x : j == 1 ? cw[t].y : j == 2 ? cw[t].z : cw[t].w;
+                wa[t] = mfma_dequant(P, d[t], kx);
+            }
+            v8bf xf = __builtin_bit_cast(v8bf, xs[buf][xslot(0, j)]);
+#pragma unroll
+            for (int ms = 0; ms < kTiledMS; ++ms) {
+                __builtin_amdgcn_sched_barrier(0);
+                const v8bf xn = __builtin_bit_cast(v8bf, xs[buf][xslot(ms + 1 < kTiledMS ? ms + 1 : ms, j)]);
+#pragma unroll
+                for (int t = 0; t < kTiledNT; ++t)
+                    acc[ms][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[t], xf, acc[ms][t], 0, 0, 0);
+                xf = xn;
+            }
+        }
+    };
+
+    // Pipeline: group kb's x tile and weights were issued one step earlier
+    // (all straight into LDS); each step issues the next group's loads
+    // (kTiledXLoads + 2 kTiledNT memory instructions per wave), waits for the
+    // older ones, and computes.  The last group is peeled so that every load
+    // in the loop is unconditional.
+    constexpr int kIssued = kTiledXLoads + 2 * kTiledNT;
+    load_x(0, 0);
+    load_w(0, 0);
+    int kb = 0;
+    for (; kb + 1 < a.Kb; ++kb) {
+        const int buf = kb & 1;
+        load_x(kb + 1, buf ^ 1);
+        load_w(kb + 1, buf ^ 1);
+        asm volatile("s_waitcnt vmcnt(%0)" :: "n"(kIssued) : "memory");
+        __syncthreads();                      // group kb is in LDS for every wave
+        compute(buf);
+        __syncthreads();                      // everyone is done reading buf before it is refilled
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    compute(kb & 1);
+
+    // D of the 16x16 op: lane l holds rows n = 4 (l >> 4) + v of column m = l & 15
+#pragma unroll
+    for (int ms = 0; ms < kTiledMS; ++ms) {
+        const int row = im * kTiledBM + ms * 16 + lm;
+        if (row >= a.M) continue;
+#pragma unroll
+        for (int t = 0; t < kTiledNT; ++t) {
+            const int tt = jn * 16 + wave * kTiledNT + t;
+            if (tt >= a.Nt) continue;
+            const v4f v = acc[ms][t];
+            const uint2 o = make_uint2(cvt_pk_bf16(v[0], v[1]), cvt_pk_bf16(v[2], v[3]));
+            *(uint2 *)(a.y + (size_t)row * a.N + (size_t)tt * kTileN + 4 * lg) = o;
+        }
+    }
+}
+
+hipError_t launch_tiled(bool symmetric, const TiledArgs &a, int grid, hipStream_t st) {
+    if (symmetric) hipLaunchKernelGGL(k_tiled<true>, dim3(grid), dim3(kTiledWaves * 64), 0, st, a);
+    else hipLaunchKernelGGL(k_tiled<false>, dim3(grid), dim3(kTiledWaves * 64), 0, st, a);
+    return hipGetLastError();
+}
+
+}  // namespace qlin

@@ -192,11 +192,46 @@ def test_prefill_rows_match_oracle(M):
     lin.close()
 
 
+@pytest.mark.parametrize("M,K,N", [(1, 256, 16), (128, 1280, 512), (200, 384, 208), (300, 1152, 496),
+                                   (129, 2560, 4112)])
+def test_tiled_matches_oracle(M, K, N):
+    """The prefill kernel: partial row blocks (M % 128), partial column blocks
+    (N % 256), several groups, every output compared."""
+    c = gen.random_case(M * 3 + K + N, M, K, N, sigma=1.0)
+    lin = make(c)
+    assert_close(run(lin, c["x"], TILED), oracle(c), f"tiled M={M} K={K} N={N}")
+    lin.close()
+
+
+def test_tiled_integer_case_is_bit_exact():
+    K, N, M = 1024, 272, 130
+    rng = np.random.default_rng(5)
+    Q = rng.integers(0, 16, size=(N, K), dtype=np.uint8)
+    xi = rng.integers(-1, 2, size=(M, K))
+    x = np.select([xi == 1, xi == -1], [0x3F80, 0xBF80], 0).astype(np.uint16)
+    c = dict(K=K, N=N, packed=ref.pack_codes(Q), scales=np.full((N, K // 128), 0x3F80, np.uint16))
+    lin = make(c, symmetric=True)
+    y_ref = ref.forward(x, c["packed"], c["scales"], ref.symmetric_zeros(N, K))
+    assert np.array_equal(run(lin, x, TILED), ref.round_output(y_ref))
+    lin.close()
+
+
+@pytest.mark.parametrize("M", [512])
+def test_config4_prefill_down_projection_full_size(M):
+    """Chunked-prefill regime at full size (K=9728, N=2560) through the
+    automatic plan (the tiled kernel), every output compared."""
+    rng_case = gen.random_case(4000 + M, M, 9728, 2560, sigma=1.0)
+    lin = make(rng_case)
+    assert "path=tiled" in lin.plan(M)
+    assert_close(run(lin, rng_case["x"]), oracle(rng_case), f"M={M}")
+    lin.close()
+
+
 def test_symmetric_forward_matches_oracle():
     c = gen.random_case(77, 16, 2560, 1024)
     lin = make(c, symmetric=True)
     y_ref = oracle(c, symmetric=True)
-    for path, M in ((GEMV, 1), (GEMV, 2), (SKINNY, 16), (SKINNY, 3), (REGS, 1), (REGS, 16)):
+    for path, M in ((GEMV, 1), (GEMV, 2), (SKINNY, 16), (SKINNY, 3), (REGS, 1), (REGS, 16), (TILED, 16)):
         assert_close(run(lin, c["x"][:M], path), y_ref[:M], f"path={path}")
     lin.close()
 
