@@ -20,8 +20,10 @@ x and y (K*N/2 + 4*(K/128)*N + 2*M*K + 2*M*N).
 
 Other modes (not the benchmark line): ``--workload`` c0 | c2m1 | c2m4 |
 c2m8 | c2m16 | model (36 layers x 6 linears at M=16, microseconds per
-verification step); ``--calibrate-copy`` runs a plain 256 MiB device copy for
-the HBM-traffic counter calibration.
+verification step) | prefill128 | prefill512 | prefill2048 (the same linears
+at M rows, TFLOP/s and matrix-core utilisation); ``--fuse-qkv`` runs the
+q, k, v projections of a layer as one launch; ``--calibrate-copy`` runs a
+plain 256 MiB device copy for the HBM-traffic counter calibration.
 """
 
 import argparse
@@ -36,6 +38,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0          # dense bf16 matrix-core peak of MI355X
 METRIC = "W4A16 linear HBM GB/s (% of peak) at M=1/16; µs per 4B-shaped layer"
 
 
@@ -146,32 +149,45 @@ def calibrate_copy():
                       "bytes_written_per_launch": 1 << 28, "launches": 20}), flush=True)
 
 
-def bench_model(args):
-    """36 layers x (q, k, v, o, gate_up, down) at M=16: one graph per step."""
+def bench_model(args, M=16, x_seed=3, fuse_qkv=False):
+    """36 layers x (q, k, v, o, gate_up, down) at M rows: one graph per step.
+    With fuse_qkv the q, k and v weights of a layer are concatenated along N
+    into one handle (the three share their input), so a layer takes four
+    launches instead of six; the outputs are the same columns."""
     import torch
 
     from paper_2607_04244_amd import qlin
     from synth import gen
     torch.cuda.set_device(0)
-    M = 16
-    lins, xs, ys, total = [], {}, [], 0
+    lins, xs, ys, total, flops = [], {}, [], 0, 0
     for layer in range(gen.N_LAYERS):
-        for p in range(len(gen.LAYER_SHAPES)):
-            w = gen.model_linear(layer, p)
+        ws = [gen.model_linear(layer, p) for p in range(len(gen.LAYER_SHAPES))]
+        if fuse_qkv:
+            qkv = dict(K=ws[0]["K"], N=sum(w["N"] for w in ws[:3]),
+                       packed=np.concatenate([w["packed"] for w in ws[:3]]),
+                       scales=np.concatenate([w["scales"] for w in ws[:3]]),
+                       zeros=np.concatenate([w["zeros"] for w in ws[:3]]))
+            ws = [qkv] + ws[3:]
+        for w in ws:
             lins.append(qlin.QLinear(w["packed"], w["scales"], w["zeros"]))
             K, N = w["K"], w["N"]
             if K not in xs:
-                xs[K] = torch.from_numpy(gen.model_activations(3, M, K).view(np.int16)).view(torch.bfloat16).cuda()
+                xs[K] = torch.from_numpy(gen.model_activations(x_seed, M, K).view(np.int16)).view(torch.bfloat16).cuda()
             ys.append(torch.empty((M, N), dtype=torch.bfloat16, device="cuda"))
             total += algorithmic_bytes(M, K, N)
+            flops += 2 * M * K * N
     stream = torch.cuda.Stream()
     calls = [(lambda l=l, y=y: l.forward(xs[l.K], out=y)) for l, y in zip(lins, ys)]
-    us_per_launch, g = graph_time_us(torch, stream, calls, reps=max(1, args.steps // 216))
+    us_per_launch, g = graph_time_us(torch, stream, calls, reps=max(1, args.steps // len(calls)))
     us_step = us_per_launch * len(calls)
-    out = {"workload": "36-layer 4B decoder weight pass M=16 (216 linears, one graph)",
+    tfs = flops / (us_step * 1e-6) / 1e12
+    out = {"workload": f"36-layer 4B decoder weight pass M={M} ({len(calls)} launches"
+                       f"{', fused qkv' if fuse_qkv else ''}, one graph)",
            "us_per_step": round(us_step, 2), "us_per_layer": round(us_step / gen.N_LAYERS, 3),
            "bytes_per_step": total, "GBps": round(total / (us_step * 1e-6) / 1e9, 1),
-           "pct_of_peak_hbm": round(100 * total / (us_step * 1e-6) / 1e9 / PEAK_HBM_GBS, 2)}
+           "pct_of_peak_hbm": round(100 * total / (us_step * 1e-6) / 1e9 / PEAK_HBM_GBS, 2),
+           "TFLOPs": round(tfs, 1), "mfma_util_pct": round(100 * tfs / PEAK_BF16_TFLOPS, 2),
+           "plans": sorted({l.plan(M) for l in lins})}
     print(json.dumps(out), flush=True)
 
 
@@ -185,6 +201,7 @@ def main():
     ap.add_argument("--split", type=int, default=0, help="force a K split (tuning)")
     ap.add_argument("--workload", default="verify")
     ap.add_argument("--calibrate-copy", action="store_true")
+    ap.add_argument("--fuse-qkv", action="store_true", help="model / prefill passes: one q|k|v launch per layer")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the layer has no multi-GPU path in this build "
@@ -192,8 +209,11 @@ def main():
         sys.exit(2)
     if args.calibrate_copy:
         return calibrate_copy()
+    if args.workload.startswith("prefill"):
+        # chunked-prefill regime: M rows through every linear of the model
+        return bench_model(args, M=int(args.workload[len("prefill"):]), x_seed=4, fuse_qkv=args.fuse_qkv)
     if args.workload == "model":
-        return bench_model(args)
+        return bench_model(args, fuse_qkv=args.fuse_qkv)
 
     import torch
 

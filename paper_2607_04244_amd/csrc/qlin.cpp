@@ -265,13 +265,20 @@ int make_tiled_plan(const qlin_s *h, int64_t split_k, int64_t M, Plan *p) {
     return QLIN_OK;
 }
 
-// Rows from which qlin_forward uses the TILED kernel instead of 64-row
-// slices of the decode kernels.
-constexpr int64_t kTiledFromM = kMaxSkinnyM + 1;
+// Does the automatic choice run M rows through the TILED kernel (one
+// launch) rather than 64-row slices of the decode kernels?  Measured on
+// MI355X: the tiled kernel wins once it has enough output blocks to spread
+// (about 64, or 16 from M = 256 on); narrow layers at M = 128 (k, v, o, down)
+// are faster as two slices.
+bool auto_tiled(const qlin_s *h, int64_t M) {
+    if (M <= kMaxSkinnyM) return false;
+    const int64_t blocks = ((M + kTiledBM - 1) / kTiledBM) * ((h->Nt + 15) / 16);
+    return blocks >= 64 || (M >= 256 && blocks >= 16);
+}
 
 int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
     const bool auto_pick = path == kAuto;
-    if (path == kTiled || (path == kAuto && M >= kTiledFromM)) return make_tiled_plan(h, split_k, M, p);
+    if (path == kTiled) return make_tiled_plan(h, split_k, M, p);
     if (path == kAuto) path = (M <= gemv_max_auto()) ? kGemv : kSkinny;
     if (path != kGemv && path != kSkinny && path != kRegs) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
     if (path == kGemv && M > kMaxGemvM) return fail(QLIN_ERR_UNSUPPORTED, "GEMV path needs M <= %d", kMaxGemvM);
@@ -367,7 +374,7 @@ int run_forward(qlin_s *h, int path, int64_t split_k, int64_t M, const uint16_t 
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
     if (dev != h->device) return fail(QLIN_ERR_INVALID, "handle belongs to device %d, current is %d", h->device, dev);
     hipStream_t st = (hipStream_t)stream;
-    if (path == kTiled || (path == kAuto && M >= kTiledFromM)) {
+    if (path == kTiled || (path == kAuto && auto_tiled(h, M))) {
         Plan p;
         rc = make_tiled_plan(h, split_k, M, &p);
         if (rc != QLIN_OK) return rc;
@@ -456,7 +463,7 @@ int qlin_plan(qlin_t h, int path, int64_t split_k, int64_t M, char *buf, int64_t
     if (path == kSkinny && M > kMaxSkinnyM) return fail(QLIN_ERR_UNSUPPORTED, "SKINNY path needs M <= 64");
     if (path == kRegs && M > 16) return fail(QLIN_ERR_UNSUPPORTED, "REGS path needs M <= 16");
     Plan p;
-    const bool tiled = path == kTiled || (path == kAuto && M >= kTiledFromM);
+    const bool tiled = path == kTiled || (path == kAuto && auto_tiled(h, M));
     int rc = tiled ? make_tiled_plan(h, split_k, M, &p) : make_plan(h, path, split_k, std::min<int64_t>(M, kMaxSkinnyM), &p);
     if (rc != QLIN_OK) return rc;
     const int64_t slices = tiled ? 1 : (M + kMaxSkinnyM - 1) / kMaxSkinnyM;

@@ -57,13 +57,15 @@ struct FwdArgs {
 static_assert((kWaves & (kWaves - 1)) == 0, "waves per workgroup must be a power of two");
 
 // TILED kernel (prefill-sized M): a workgroup of kTiledWaves waves computes
-// kTiledBM rows x kTiledBN columns; each wave owns kTiledNT column tiles.
-constexpr int kTiledWaves = 4;
+// kTiledBM rows x kTiledBN columns; wave (wm, wn) owns kTiledNT column tiles
+// and kTiledMSW m-subtiles of 16 rows.
+constexpr int kTiledWaves = 8;
 constexpr int kTiledNT = 4;
 constexpr int kTiledBM = 128;
-constexpr int kTiledMS = kTiledBM / 16;                    // 16-row m-subtiles
-constexpr int kTiledBN = kTiledWaves * kTiledNT * kTileN;  // 256 columns
+constexpr int kTiledMSW = kTiledBM / 16 / 2;               // 4: two waves per tile set
+constexpr int kTiledBN = 4 * kTiledNT * kTileN;            // 256 columns
 constexpr int kTiledXLoads = kTiledBM * 16 / (kTiledWaves * 64);   // direct-to-LDS loads per wave and group
+constexpr int kTiledStages = 3;                            // LDS pipeline depth (groups)
 
 struct TiledArgs {
     const uint4 *codes;

@@ -13,15 +13,17 @@ namespace qlin {
 
 // ---- TILED: prefill-sized M (GEMM), matrix-core dequantization ----------
 //
-// A workgroup of kTiledWaves waves computes a kTiledBM x kTiledBN block of y:
-// rows [128 im, 128 im + 128) and column tiles [16 jn, 16 jn + 16); wave w
-// owns tiles 16 jn + 4 w + t, t < 4, for all 128 rows.  Per group kb the
-// workgroup stages the 128 x 128 x-tile in LDS with direct-to-LDS loads
-// (global_load_lds_dwordx4, no VGPR round trip), double-buffered one group
-// ahead, and each wave loads its four weight blocks one group ahead into
-// registers.  Dequantization (the matrix-core route) produces the A operand
-// of v_mfma_f32_16x16x32_bf16 directly; each x fragment read from LDS feeds
-// the four tiles of the wave.
+// A workgroup of kTiledWaves = 8 waves computes a kTiledBM x kTiledBN = 128 x
+// 256 block of y: rows [128 im, 128 im + 128), column tiles [16 jn, 16 jn +
+// 16).  Wave (wm, wn) = (w >> 2, w & 3) owns rows [64 wm, 64 wm + 64) (four
+// m-subtiles of 16) of the four tiles 4 wn + t, t < 4: two waves share each
+// tile set and sit on one SIMD, so while one dequantizes (vector ALU) the
+// other's matrix products run.  Per group kb the workgroup stages the
+// 128 x 128 x-tile and the 16 weight blocks (plus their scales) in LDS with
+// direct-to-LDS loads (global_load_lds, no VGPR round trip), kTiledStages
+// groups deep.  Dequantization (the matrix-core route) produces the A
+// operand of v_mfma_f32_16x16x32_bf16 directly; each x fragment read from
+// LDS feeds the four tiles of the wave.
 //
 // x tile in LDS: 16-byte chunk (row r, c) = x[row][128 kb + 8c .. + 8],
 // c < 16, at slot 16 r + (c ^ (r & 15)): a wave's direct-to-LDS load fills 64
@@ -38,15 +40,17 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 typedef __attribute__((address_space(1))) void glb_void_t;
 
 template <bool SYM>
-__global__ void __launch_bounds__(kTiledWaves * 64, 1) k_tiled(TiledArgs a) {
-    __shared__ __align__(16) uint4 xs[2][kTiledBM * 16];
-    // weight blocks of the workgroup's 16 tiles (wave w: tiles 4 w .. 4 w + 3,
-    // 1 KiB each) and their s|z words (64 per tile; lane l of a load writes
-    // the word of column l & 15, the other 48 are copies), double-buffered
-    __shared__ __align__(16) uint4 ws_codes[2][kTiledWaves * kTiledNT * 64];
-    __shared__ __align__(16) uint32_t ws_sz[2][kTiledWaves * kTiledNT * 64];
+__global__ void __launch_bounds__(kTiledWaves * 64, 2) k_tiled(TiledArgs a) {
+    constexpr int kTiles = kTiledBN / kTileN;            // 16 tiles per workgroup
+    __shared__ __align__(16) uint4 xs[kTiledStages][kTiledBM * 16];
+    // the workgroup's 16 weight blocks (1 KiB each) and their s|z words (64
+    // per tile: lane l of a load writes the word of column l & 15, the other
+    // 48 are copies), one buffer per pipeline stage
+    __shared__ __align__(16) uint4 ws_codes[kTiledStages][kTiles * 64];
+    __shared__ __align__(16) uint32_t ws_sz[kTiledStages][kTiles * 64];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave >> 2, wn = wave & 3;
     const ExtractConsts kx;
     // block index -> (column block jn, row block im)
     const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3;
@@ -57,40 +61,40 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 1) k_tiled(TiledArgs a) {
     const int lm = lane & 15, lg = lane >> 4;
     const uint32_t shift = (lane & 1) * 16, keep_lo = (lane & 2) ? 0u : 0xFFFFFFFFu;
 
-    // element offsets (from x, group 0) of this lane's direct-to-LDS loads:
-    // load i of wave w fills rows 32 w + 4 i + (lane >> 4), slot position
+    // x: load i of wave w fills rows 16 w + 4 i + (lane >> 4), slot position
     // lane & 15, which holds chunk (lane & 15) ^ (row & 15) of that row.
-    // The planner keeps M * K below 2^31.
+    // Element offsets from x at group 0; the planner keeps M * K below 2^31.
+    constexpr int kRowsPerWave = kTiledBM / kTiledWaves;     // 16
     uint32_t xo[kTiledXLoads];
 #pragma unroll
     for (int i = 0; i < kTiledXLoads; ++i) {
-        const int r = wave * (kTiledBM / kTiledWaves) + 4 * i + lg;
+        const int r = wave * kRowsPerWave + 4 * i + lg;
         const int row = min(im * kTiledBM + r, a.M - 1);
         xo[i] = (uint32_t)row * (uint32_t)a.K + (uint32_t)(((lane & 15) ^ (r & 15)) * 8);
     }
     auto load_x = [&](int kb, int buf) {
 #pragma unroll
-        for (int i = 0; i < kTiledXLoads; ++i) {
-            const int r0 = wave * (kTiledBM / kTiledWaves) + 4 * i;
+        for (int i = 0; i < kTiledXLoads; ++i)
             __builtin_amdgcn_global_load_lds((glb_void_t *)(a.x + xo[i] + (uint32_t)kb * kGroup),
-                                             (lds_void_t *)&xs[buf][r0 * 16], 16, 0, 0);
-        }
+                                             (lds_void_t *)&xs[buf][(wave * kRowsPerWave + 4 * i) * 16], 16, 0, 0);
     };
-    // this wave's four tiles (clamped for loads): uint4 index of block (t, 0)
-    uint32_t wo[kTiledNT];
+    // weights: wave (wm, wn) loads tiles 4 wn + 2 wm + u, u < 2 (clamped to
+    // the last tile); wo = uint4 index of block (tile, 0) / 64
+    constexpr int kWLoads = kTiles / kTiledWaves;            // 2 tiles per wave
+    uint32_t wo[kWLoads];
 #pragma unroll
-    for (int t = 0; t < kTiledNT; ++t)
-        wo[t] = (uint32_t)min(jn * 16 + wave * kTiledNT + t, a.Nt - 1) * (uint32_t)a.Kb;
+    for (int u = 0; u < kWLoads; ++u)
+        wo[u] = (uint32_t)min(jn * kTiles + wn * kTiledNT + kWLoads * wm + u, a.Nt - 1) * (uint32_t)a.Kb;
     auto load_w = [&](int kb, int buf) {
 #pragma unroll
-        for (int t = 0; t < kTiledNT; ++t) {
-            const uint32_t b = wo[t] + (uint32_t)kb;
-            const int slot = (wave * kTiledNT + t) * 64;
+        for (int u = 0; u < kWLoads; ++u) {
+            const uint32_t b = wo[u] + (uint32_t)kb;
+            const int slot = (wn * kTiledNT + kWLoads * wm + u) * 64;
             __builtin_amdgcn_global_load_lds((glb_void_t *)(a.codes + (size_t)b * 64 + lane),
                                              (lds_void_t *)&ws_codes[buf][slot], 16, 0, 0);
             if constexpr (SYM) {
                 // 2-byte scales: one dword per lane covers columns 2i, 2i + 1;
-                // lane l & 7 then picks its half below
+                // read_w picks the half
                 __builtin_amdgcn_global_load_lds((glb_void_t *)((const uint32_t *)a.sz + (size_t)b * (kTileN / 2) + (lane & 7)),
                                                  (lds_void_t *)&ws_sz[buf][slot], 4, 0, 0);
             } else {
@@ -99,11 +103,11 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 1) k_tiled(TiledArgs a) {
             }
         }
     };
-    // this lane's code words and s|z word of tile t from LDS
+    // this lane's code words and s|z word of the wave's tile t from LDS
     auto read_w = [&](int buf, uint4 (&cw)[kTiledNT], uint32_t (&sw)[kTiledNT]) {
 #pragma unroll
         for (int t = 0; t < kTiledNT; ++t) {
-            const int slot = (wave * kTiledNT + t) * 64;
+            const int slot = (wn * kTiledNT + t) * 64;
             cw[t] = ws_codes[buf][slot + lane];
             if constexpr (SYM) {
                 const uint32_t pair = ws_sz[buf][slot + (lm >> 1)];
@@ -114,14 +118,14 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 1) k_tiled(TiledArgs a) {
         }
     };
 
-    v4f acc[kTiledMS][kTiledNT];
+    v4f acc[kTiledMSW][kTiledNT];
 #pragma unroll
-    for (int ms = 0; ms < kTiledMS; ++ms)
+    for (int ms = 0; ms < kTiledMSW; ++ms)
 #pragma unroll
         for (int t = 0; t < kTiledNT; ++t) acc[ms][t] = v4f{0, 0, 0, 0};
 
-    // LDS slot of this lane's operand read (row 16 ms + lm, chunk 4 j + lg)
-    auto xslot = [&](int ms, int j) { return ms * 256 + lm * 16 + ((4 * j + lg) ^ lm); };
+    // LDS slot of this lane's operand read: row 64 wm + 16 ms + lm, chunk 4 j + lg
+    auto xslot = [&](int ms, int j) { return (kTiledMSW * wm + ms) * 256 + lm * 16 + ((4 * j + lg) ^ lm); };
 
     auto compute = [&](int buf) {
         uint4 cw[kTiledNT];
@@ -132,59 +136,55 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 1) k_tiled(TiledArgs a) {
         for (int t = 0; t < kTiledNT; ++t) d[t] = mfma_setup(sw[t], shift, keep_lo);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            // one k-step of 32 at a time, and x fragments read one m-subtile
-            // ahead of their products: bounds the live registers so that the
-            // accumulators and operands fit the VGPR file
-            __builtin_amdgcn_sched_barrier(0);
             v8bf wa[kTiledNT];
 #pragma unroll
             for (int t = 0; t < kTiledNT; ++t) {
                 const uint32_t P = j == 0 ? cw[t].x : j == 1 ? cw[t].y : j == 2 ? cw[t].z : cw[t].w;
                 wa[t] = mfma_dequant(P, d[t], kx);
             }
-            v8bf xf = __builtin_bit_cast(v8bf, xs[buf][xslot(0, j)]);
 #pragma unroll
-            for (int ms = 0; ms < kTiledMS; ++ms) {
-                __builtin_amdgcn_sched_barrier(0);
-                const v8bf xn = __builtin_bit_cast(v8bf, xs[buf][xslot(ms + 1 < kTiledMS ? ms + 1 : ms, j)]);
+            for (int ms = 0; ms < kTiledMSW; ++ms) {
+                const v8bf xf = __builtin_bit_cast(v8bf, xs[buf][xslot(ms, j)]);
 #pragma unroll
                 for (int t = 0; t < kTiledNT; ++t)
                     acc[ms][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[t], xf, acc[ms][t], 0, 0, 0);
-                xf = xn;
             }
         }
     };
 
-    // Pipeline: group kb's x tile and weights were issued one step earlier
-    // (all straight into LDS); each step issues the next group's loads
-    // (kTiledXLoads + 2 kTiledNT memory instructions per wave), waits for the
-    // older ones, and computes.  The last group is peeled so that every load
-    // in the loop is unconditional.
-    constexpr int kIssued = kTiledXLoads + 2 * kTiledNT;
-    load_x(0, 0);
-    load_w(0, 0);
-    int kb = 0;
-    for (; kb + 1 < a.Kb; ++kb) {
-        const int buf = kb & 1;
-        load_x(kb + 1, buf ^ 1);
-        load_w(kb + 1, buf ^ 1);
-        asm volatile("s_waitcnt vmcnt(%0)" :: "n"(kIssued) : "memory");
+    // Pipeline of kTiledStages LDS buffers: groups kb + 1 .. kb + S - 1 are
+    // in flight (straight into LDS) while group kb is computed.  Each step
+    // issues one group's loads (kIssued memory instructions per wave; past
+    // the last group they reload it into a buffer nobody reads), waits for
+    // group kb's, and computes it.
+    constexpr int kIssued = kTiledXLoads + 2 * kWLoads;
+    constexpr int S = kTiledStages;
+#pragma unroll
+    for (int i = 0; i < S - 1; ++i) {
+        load_x(min(i, a.Kb - 1), i);
+        load_w(min(i, a.Kb - 1), i);
+    }
+    int buf = 0;
+    for (int kb = 0; kb < a.Kb; ++kb) {
+        const int nb = buf == 0 ? S - 1 : buf - 1;             // (kb + S - 1) % S
+        load_x(min(kb + S - 1, a.Kb - 1), nb);
+        load_w(min(kb + S - 1, a.Kb - 1), nb);
+        asm volatile("s_waitcnt vmcnt(%0)" :: "n"((S - 1) * kIssued) : "memory");
         __syncthreads();                      // group kb is in LDS for every wave
         compute(buf);
         __syncthreads();                      // everyone is done reading buf before it is refilled
+        buf = buf == S - 1 ? 0 : buf + 1;
     }
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    __syncthreads();
-    compute(kb & 1);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the reloads past the end
 
     // D of the 16x16 op: lane l holds rows n = 4 (l >> 4) + v of column m = l & 15
 #pragma unroll
-    for (int ms = 0; ms < kTiledMS; ++ms) {
-        const int row = im * kTiledBM + ms * 16 + lm;
+    for (int ms = 0; ms < kTiledMSW; ++ms) {
+        const int row = im * kTiledBM + (kTiledMSW * wm + ms) * 16 + lm;
         if (row >= a.M) continue;
 #pragma unroll
         for (int t = 0; t < kTiledNT; ++t) {
-            const int tt = jn * 16 + wave * kTiledNT + t;
+            const int tt = jn * kTiles + wn * kTiledNT + t;
             if (tt >= a.Nt) continue;
             const v4f v = acc[ms][t];
             const uint2 o = make_uint2(cvt_pk_bf16(v[0], v[1]), cvt_pk_bf16(v[2], v[3]));
