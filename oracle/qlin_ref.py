@@ -154,6 +154,37 @@ def symmetric_zeros(N, K, group=GROUP):
 # the linear layer
 # --------------------------------------------------------------------------
 
+def quantize_rtn(w_bits, scales, zeros, group=GROUP):
+    """Fixed-grid round-to-nearest quantization of bf16 weights.
+
+    Sec. 2.1 (QAD paragraph): at packing time the trained bf16 weights are
+    rounded back onto the quantization grid of the frozen scales, giving new
+    4-bit codes under the same scales; Sec. 4 (drafter PTQ, Table of drafter
+    quantizers): round-to-nearest is the RTN baseline.  With the unsigned
+    codes of this build (signed code = q - z):
+
+        code[n][k] = clamp(round(w[n][k] / s[n][g]) + z[n][g], 0, 15),  g = k // group
+
+    Readings (the paper fixes neither): the quotient is formed in binary32
+    (IEEE division, correctly rounded) and rounded to the nearest integer with
+    ties to even; a NaN quotient (0/0) gives code z.  Returns uint8 [N][K].
+    """
+    w = bf16_to_f64(w_bits).astype(np.float32)
+    s = np.repeat(bf16_to_f64(scales).astype(np.float32), group, axis=1)
+    z = np.repeat(bf16_to_f64(zeros), group, axis=1)
+    with np.errstate(divide="ignore", invalid="ignore", over="ignore"):
+        qf = w / s                                  # binary32 / binary32 -> binary32
+        r = np.rint(qf).astype(np.float64)          # nearest integer, ties to even
+    code = np.clip(r + z, 0.0, 15.0)
+    code = np.where(np.isnan(code), z, code)
+    return code.astype(np.uint8)
+
+
+def quantize_pack(w_bits, scales, zeros, group=GROUP):
+    """quantize_rtn() followed by the [N][K/8] packing of pack_codes()."""
+    return pack_codes(quantize_rtn(w_bits, scales, zeros, group))
+
+
 def forward(x_bits, packed, scales, zeros, group=GROUP, mode="bf16"):
     """y[M][N] = x[M][K] . w[N][K]^T in float64.
 

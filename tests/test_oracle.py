@@ -310,3 +310,60 @@ def test_generator_is_seeded():
     for k in ("packed", "scales", "zeros", "x"):
         assert np.array_equal(a[k], b[k])
     assert a["x"].shape == (1, 2560) and a["packed"].shape == (2560, 320)
+
+
+# ---------------------------------------------------------------- fixed-grid RTN quantization
+
+def _rtn_fixture():
+    import json
+    import os
+    with open(os.path.join(os.path.dirname(__file__), "golden", "rtn_rounding.json")) as f:
+        return json.load(f)["cases"]
+
+
+def test_rtn_golden_rounding():
+    """Hand-worked ties, zero-points and clamps (golden fixture)."""
+    for c in _rtn_fixture():
+        w = np.full((1, 128), int(c["w"], 16), np.uint16)
+        s = np.array([[int(c["s"], 16)]], np.uint16)
+        z = ref.rne_bf16(np.array([[float(c["z"])]]))
+        q = ref.quantize_rtn(w, s, z)
+        assert np.all(q == c["code"]), c
+
+
+def test_rtn_inverts_dequantization_exhaustively():
+    """quantize(dequant(q)) == q for every code and zero-point over every
+    positive normal bf16 scale in [2^-100, 2^100]: the bf16 rounding of
+    (q - z) s moves the quotient by at most 15 * 2^-9 < 1/2."""
+    sb = np.arange(0x0000, 0x8000, dtype=np.uint32).astype(np.uint16)
+    sv = ref.bf16_to_f64(sb)
+    sb = sb[(sv >= 2.0 ** -100) & (sv <= 2.0 ** 100)]
+    q = np.arange(16, dtype=np.uint8)
+    for z in range(16):
+        zz = ref.rne_bf16(np.full((sb.size, 1), float(z)))
+        # one row per scale, one group of 128 columns holding every code 8 times
+        codes = np.tile(np.repeat(q, 8), (sb.size, 1))
+        packed = ref.pack_codes(codes)
+        w = ref.dequant_bf16(packed, sb.reshape(-1, 1), zz)
+        assert np.array_equal(ref.quantize_rtn(w, sb.reshape(-1, 1), zz), codes), f"z={z}"
+
+
+def test_rtn_is_monotone_and_clamped():
+    """Codes never decrease as w grows (fixed s, z) and stay in [0, 15]."""
+    wv = np.linspace(-40.0, 40.0, 4096).astype(np.float32).astype(np.float64)
+    wb = ref.rne_bf16(wv).reshape(32, 128)          # rounding keeps the order
+    for s_val, z in ((1.0, 8), (0.375, 3), (2.5, 12)):
+        s = np.repeat(ref.rne_bf16(np.array([[s_val]])), 32, 0)
+        zz = np.repeat(ref.rne_bf16(np.array([[float(z)]])), 32, 0)
+        q = ref.quantize_rtn(wb, s, zz).ravel()
+        assert np.all(np.diff(q.astype(int)) >= 0) and q.min() == 0 and q.max() == 15
+
+
+def test_rtn_nan_quotient_gives_zero_point_and_pack_layout():
+    w = np.zeros((2, 128), np.uint16)                      # w = 0
+    s = np.array([[0x0000], [0x3F80]], np.uint16)          # s = 0 (0/0 = NaN), s = 1
+    z = ref.rne_bf16(np.array([[5.0], [9.0]]))
+    q = ref.quantize_rtn(w, s, z)
+    assert np.all(q[0] == 5) and np.all(q[1] == 9)
+    p = ref.quantize_pack(w, s, z)
+    assert p.shape == (2, 16) and np.all(p[0] == 0x55555555) and np.all(p[1] == 0x99999999)
