@@ -21,7 +21,8 @@ x and y (K*N/2 + 4*(K/128)*N + 2*M*K + 2*M*N).
 Other modes (not the benchmark line): ``--workload`` c0 | c2m1 | c2m4 |
 c2m8 | c2m16 | model (36 layers x 6 linears at M=16, microseconds per
 verification step) | prefill128 | prefill512 | prefill2048 (the same linears
-at M rows, TFLOP/s and matrix-core utilisation); ``--fuse-qkv`` runs the
+at M rows, TFLOP/s and matrix-core utilisation) | quantize (bf16 -> packed
+int4 codes on a fixed grid, GB/s); ``--fuse-qkv`` runs the
 q, k, v projections of a layer as one launch; ``--calibrate-copy`` runs a
 plain 256 MiB device copy for the HBM-traffic counter calibration.
 """
@@ -191,6 +192,33 @@ def bench_model(args, M=16, x_seed=3, fuse_qkv=False):
     print(json.dumps(out), flush=True)
 
 
+def bench_quantize(args):
+    """Fixed-grid RTN quantize + pack of the fused gate+up weight (N = 19456,
+    K = 2560) from bf16: HBM-bound, reports GB/s of algorithmic bytes (bf16
+    weights in, packed codes out, scales and zeros in)."""
+    import torch
+
+    from paper_2607_04244_amd import qlin
+    torch.cuda.set_device(0)
+    N, K = 19456, 2560
+    rng = np.random.default_rng(5)
+    g = torch.Generator(device="cuda").manual_seed(5)
+    ws = [torch.randn((N, K), device="cuda", generator=g).mul_(0.02).to(torch.bfloat16) for _ in range(12)]
+    sc = torch.from_numpy(rng.uniform(0.002, 0.02, size=(N, K // 128)).astype(np.float32)).to(torch.bfloat16).cuda()
+    zr = torch.from_numpy(rng.integers(7, 10, size=(N, K // 128)).astype(np.float32)).to(torch.bfloat16).cuda()
+    out = torch.empty((N, K // 8), dtype=torch.int32, device="cuda")
+    nbytes = N * K * 2 + N * K // 2 + 4 * N * (K // 128)
+    stream = torch.cuda.Stream()
+    calls = [(lambda w=w: qlin._check(qlin.qlin_quantize(K, N, 128, w.data_ptr(), sc.data_ptr(), zr.data_ptr(),
+                                                       out.data_ptr(), torch.cuda.current_stream().cuda_stream)))
+             for w in ws]
+    us, _ = graph_time_us(torch, stream, calls, reps=max(1, args.steps // len(calls)))
+    print(json.dumps({"workload": f"quantize+pack N={N} K={K} bf16 -> int4 g128 (12 rotating weight copies)",
+                      "us_per_call": round(us, 3), "bytes_per_call": nbytes,
+                      "GBps": round(nbytes / (us * 1e-6) / 1e9, 1),
+                      "pct_of_peak_hbm": round(100 * nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 2)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -214,6 +242,8 @@ def main():
         return bench_model(args, M=int(args.workload[len("prefill"):]), x_seed=4, fuse_qkv=args.fuse_qkv)
     if args.workload == "model":
         return bench_model(args, fuse_qkv=args.fuse_qkv)
+    if args.workload == "quantize":
+        return bench_quantize(args)
 
     import torch
 

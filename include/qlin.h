@@ -57,11 +57,14 @@ enum {
 /*
  * qlin_create -- build a handle for one linear layer (K inputs, N outputs).
  *
- *   packed_w  HOST  uint32 [N][K/8]; code of (n, k = 8j + i) is
- *                   (packed_w[n*K/8 + j] >> 4i) & 0xF (lowest nibble = lowest k)
- *   scales    HOST  bf16 [N][K/group]; positive normal numbers in [2^-100, 2^100]
- *   zeros     HOST  bf16 [N][K/group]; integer values in [0, 15]
+ *   packed_w  uint32 [N][K/8]; code of (n, k = 8j + i) is
+ *             (packed_w[n*K/8 + j] >> 4i) & 0xF (lowest nibble = lowest k)
+ *   scales    bf16 [N][K/group]; positive normal numbers in [2^-100, 2^100]
+ *   zeros     bf16 [N][K/group]; integer values in [0, 15]
  *   group     must be 128 (Sec. 3.3)
+ * Each of the three may be host memory or device memory of the current
+ * device (such as qlin_quantize's output); device scales and zero-points are
+ * copied to the host for the checks.
  *
  * Constraints: K > 0, N > 0, K % 128 == 0, N % 16 == 0, K <= 65536,
  * N <= 1048576.  The call copies and re-lays-out the weights into device
@@ -82,6 +85,29 @@ qlin_t qlin_create(int64_t K, int64_t N, int64_t group,
  */
 qlin_t qlin_create_symmetric(int64_t K, int64_t N, int64_t group,
                              const uint32_t *packed_w, const uint16_t *scales);
+
+/*
+ * qlin_quantize -- round bf16 weights onto a fixed quantization grid and pack
+ * the codes (Sec. 2.1: at packing time the trained bf16 weights are rounded
+ * back onto the grid of the frozen scales; Sec. 4: the round-to-nearest
+ * quantizer of the drafter comparison):
+ *   code[n][k] = clamp(rint(w[n][k] / s[n][k/128]) + z[n][k/128], 0, 15)
+ * The quotient is a correctly rounded binary32 division, rint rounds to the
+ * nearest integer with ties to even, and a NaN quotient gives z.
+ *
+ *   w       DEVICE bf16 [N][K], 16-byte aligned
+ *   scales  DEVICE bf16 [N][K/group]; positive for a meaningful grid
+ *   zeros   DEVICE bf16 [N][K/group] integers in [0, 15], or NULL for the
+ *           symmetric format (z = 8)
+ *   packed  DEVICE uint32 [N][K/8] output in qlin_create's layout, 4-byte
+ *           aligned, must not overlap w
+ *   stream  hipStream_t; NULL = the default stream
+ *
+ * Shape rules as qlin_create.  Asynchronous.  Errors: INVALID (shape, NULL,
+ * overlap), UNSUPPORTED (group, N % 16, limits), ALIGN, HIP.
+ */
+int qlin_quantize(int64_t K, int64_t N, int64_t group, const uint16_t *w, const uint16_t *scales,
+                  const uint16_t *zeros, uint32_t *packed, void *stream);
 
 /*
  * qlin_forward -- y[M][N] = x[M][K] . w^T as defined above (asynchronous).

@@ -32,6 +32,7 @@
 
 #include "device_common.h"
 
+#include <algorithm>
 #include <cstdio>
 
 namespace qlin {
@@ -769,6 +770,51 @@ __global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
     }
     lds_barrier();
     write_out_waves<TN>(a, w, slots, MV);
+}
+
+// ------------------------------------------------------------------ quantize + pack
+
+// Fixed-grid round-to-nearest quantization of bf16 weights and packing into
+// the canonical [N][K/8] words (Sec. 2.1: at packing time the trained bf16
+// weights are rounded back onto the grid of the frozen scales; Sec. 4: the
+// RTN quantizer):  code = clamp(rint(w / s) + z, 0, 15), quotient in binary32
+// with a correctly rounded division, nearest integer with ties to even, a
+// NaN quotient gives z; code k = 8j + i goes to bits [4i, 4i + 4) of word j.
+// One thread per output word: a 16-byte load of 8 weights, one 4-byte store.
+template <bool SYM>
+__global__ void k_quantize_pack(const uint4 *__restrict__ w, const uint16_t *__restrict__ scales,
+                                const uint16_t *__restrict__ zeros, uint32_t *__restrict__ packed, int K, int N) {
+    const int K8 = K / 8, Kg = K / kGroup;
+    const size_t total = (size_t)N * K8;
+    for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
+         idx += (size_t)gridDim.x * blockDim.x) {
+        const size_t n = idx / K8;
+        const int j = (int)(idx - n * K8);
+        const size_t g = n * Kg + (size_t)(j / (kGroup / 8));
+        const float s = __uint_as_float((uint32_t)scales[g] << 16);
+        const float z = SYM ? 8.0f : __uint_as_float((uint32_t)zeros[g] << 16);
+        const uint4 v = w[idx];
+        const uint32_t half[4] = {v.x, v.y, v.z, v.w};
+        uint32_t word = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const uint32_t b = (i & 1) ? (half[i >> 1] & 0xFFFF0000u) : (half[i >> 1] << 16);
+            const float qf = __fdiv_rn(__uint_as_float(b), s);
+            float c = __builtin_rintf(qf) + z;
+            c = qf != qf ? z : fminf(fmaxf(c, 0.0f), 15.0f);
+            word |= (uint32_t)c << (4 * i);
+        }
+        packed[idx] = word;
+    }
+}
+
+hipError_t launch_quantize(const uint16_t *w, const uint16_t *scales, const uint16_t *zeros, uint32_t *packed,
+                           int K, int N, hipStream_t st) {
+    const size_t words = (size_t)N * (K / 8);
+    const int grid = (int)std::min<size_t>((words + 255) / 256, 65536);
+    if (zeros) hipLaunchKernelGGL(k_quantize_pack<false>, dim3(grid), dim3(256), 0, st, (const uint4 *)w, scales, zeros, packed, K, N);
+    else hipLaunchKernelGGL(k_quantize_pack<true>, dim3(grid), dim3(256), 0, st, (const uint4 *)w, scales, zeros, packed, K, N);
+    return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ measurement

@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <vector>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -87,6 +88,17 @@ int check_shape(int64_t K, int64_t N, int64_t group) {
 // Scales must be positive normal bf16 numbers in [2^-100, 2^100]: inside that
 // range every (128 + q) * s and (q - z) * s is an exact binary32 number, which
 // is what makes the matrix-core dequantization exact.
+// Is p device memory?  Pageable host memory is not known to the runtime
+// (the query fails, its error is cleared) and counts as host.
+bool is_device_ptr(const void *p) {
+    hipPointerAttribute_t attr;
+    if (hipPointerGetAttributes(&attr, p) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    return attr.type == hipMemoryTypeDevice;
+}
+
 int check_scales(const uint16_t *s, size_t n) {
     for (size_t i = 0; i < n; ++i) {
         const int e = (s[i] >> 7) & 0xFF;
@@ -137,8 +149,25 @@ qlin_t create_impl(int64_t K, int64_t N, int64_t group, const uint32_t *packed, 
         return nullptr;
     }
     const size_t ngroups = (size_t)N * (K / kGroup);
-    if (check_scales(scales, ngroups) != QLIN_OK) return nullptr;
-    if (!symmetric && check_zeros(zeros, ngroups) != QLIN_OK) return nullptr;
+    // inputs may live in device memory (e.g. written by qlin_quantize): the
+    // scale and zero-point checks then run on host copies
+    std::vector<uint16_t> s_host, z_host;
+    if (is_device_ptr(scales)) {
+        s_host.resize(ngroups);
+        if (hipMemcpy(s_host.data(), scales, ngroups * 2, hipMemcpyDeviceToHost) != hipSuccess) {
+            hip_fail(hipGetLastError(), "copy scales to host");
+            return nullptr;
+        }
+    }
+    if (!symmetric && is_device_ptr(zeros)) {
+        z_host.resize(ngroups);
+        if (hipMemcpy(z_host.data(), zeros, ngroups * 2, hipMemcpyDeviceToHost) != hipSuccess) {
+            hip_fail(hipGetLastError(), "copy zero-points to host");
+            return nullptr;
+        }
+    }
+    if (check_scales(s_host.empty() ? scales : s_host.data(), ngroups) != QLIN_OK) return nullptr;
+    if (!symmetric && check_zeros(z_host.empty() ? zeros : z_host.data(), ngroups) != QLIN_OK) return nullptr;
 
     qlin_s *h = new qlin_s;
     h->K = K;
@@ -183,11 +212,11 @@ qlin_t create_impl(int64_t K, int64_t N, int64_t group, const uint32_t *packed, 
         return bail("hipDeviceGetAttribute", e);
     static std::once_flag once;
     std::call_once(once, [] { (void)prepare_kernels(); (void)hipGetLastError(); });
-    if ((e = hipMemcpy(canon, packed, code_bytes, hipMemcpyHostToDevice)) != hipSuccess)
+    if ((e = hipMemcpy(canon, packed, code_bytes, hipMemcpyDefault)) != hipSuccess)
         return bail("copy codes", e);
-    if ((e = hipMemcpy(sc, scales, ngroups * 2, hipMemcpyHostToDevice)) != hipSuccess)
+    if ((e = hipMemcpy(sc, scales, ngroups * 2, hipMemcpyDefault)) != hipSuccess)
         return bail("copy scales", e);
-    if (!symmetric && (e = hipMemcpy(zc, zeros, ngroups * 2, hipMemcpyHostToDevice)) != hipSuccess)
+    if (!symmetric && (e = hipMemcpy(zc, zeros, ngroups * 2, hipMemcpyDefault)) != hipSuccess)
         return bail("copy zeros", e);
     if ((e = hipMemset(h->counters, 0, (size_t)h->counters_n * 4)) != hipSuccess)
         return bail("hipMemset", e);
@@ -438,6 +467,21 @@ qlin_t qlin_create(int64_t K, int64_t N, int64_t group, const uint32_t *packed_w
 qlin_t qlin_create_symmetric(int64_t K, int64_t N, int64_t group, const uint32_t *packed_w,
                              const uint16_t *scales) {
     return create_impl(K, N, group, packed_w, scales, nullptr, true);
+}
+
+int qlin_quantize(int64_t K, int64_t N, int64_t group, const uint16_t *w, const uint16_t *scales,
+                  const uint16_t *zeros, uint32_t *packed, void *stream) {
+    clear_err();
+    if (check_shape(K, N, group) != QLIN_OK) return g_status;
+    if (!w || !scales || !packed) return fail(QLIN_ERR_INVALID, "NULL pointer");
+    if (((uintptr_t)w & 15) || ((uintptr_t)packed & 3) || ((uintptr_t)scales & 1) || ((uintptr_t)zeros & 1))
+        return fail(QLIN_ERR_ALIGN, "w must be 16-byte, packed 4-byte and scales/zeros 2-byte aligned");
+    const uintptr_t wa = (uintptr_t)w, we = wa + (uintptr_t)(N * K * 2);
+    const uintptr_t pa = (uintptr_t)packed, pe = pa + (uintptr_t)(N * K / 2);
+    if (wa < pe && pa < we) return fail(QLIN_ERR_INVALID, "packed overlaps w");
+    hipError_t e = launch_quantize(w, scales, zeros, packed, (int)K, (int)N, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(e, "quantize launch");
+    return QLIN_OK;
 }
 
 int qlin_forward(qlin_t h, int64_t M, const uint16_t *x, uint16_t *y, void *stream) {

@@ -111,6 +111,8 @@ hipError_t launch_unpack(const uint4 *codes, uint8_t *q, int K, int N, hipStream
 hipError_t launch_dequant(int routine, const uint4 *codes, const void *sz, bool symmetric,
                           uint16_t *w, int K, int N, hipStream_t st);
 hipError_t prepare_kernels();     // per-process attribute setup (LDS limits)
+hipError_t launch_quantize(const uint16_t *w, const uint16_t *scales, const uint16_t *zeros, uint32_t *packed,
+                           int K, int N, hipStream_t st);
 hipError_t launch_tiled(bool symmetric, const TiledArgs &a, int grid, hipStream_t st);
 hipError_t launch_stream_read(const void *buf, size_t bytes, int grid, uint32_t *sink, hipStream_t st);
 const char *kernel_name(int kern, int mrows, int tn, bool symmetric);

@@ -26,7 +26,7 @@ PATH_AUTO, PATH_GEMV, PATH_SKINNY, PATH_TILED, PATH_REGS = 0, 1, 2, 3, 4
 # every symbol include/qlin.h declares
 EXPORTS = ("qlin_create", "qlin_create_symmetric", "qlin_forward", "qlin_forward_path",
            "qlin_plan", "qlin_destroy", "qlin_last_error", "qlin_unpack_codes",
-           "qlin_dequantize", "qlin_shape", "qlin_last_status", "qlin_stream_read")
+           "qlin_dequantize", "qlin_shape", "qlin_last_status", "qlin_stream_read", "qlin_quantize")
 
 _lib = None
 
@@ -50,6 +50,8 @@ def lib():
     L.qlin_create.argtypes = [I64, I64, I64, VP, VP, VP]
     L.qlin_create_symmetric.restype = P
     L.qlin_create_symmetric.argtypes = [I64, I64, I64, VP, VP]
+    L.qlin_quantize.restype = I32
+    L.qlin_quantize.argtypes = [I64, I64, I64, VP, VP, VP, VP, VP]
     L.qlin_forward.restype = I32
     L.qlin_forward.argtypes = [P, I64, VP, VP, VP]
     L.qlin_forward_path.restype = I32
@@ -93,8 +95,12 @@ def _check(rc):
 
 
 def _host_ptr(a, dtype):
+    """(keep-alive object, address) of a host array, or of a device tensor
+    (any object with data_ptr(), passed through as is)."""
     if a is None:
         return None, None
+    if hasattr(a, "data_ptr"):
+        return a, a.data_ptr()
     a = np.ascontiguousarray(a, dtype=dtype)
     return a, a.ctypes.data
 
@@ -119,6 +125,24 @@ def qlin_create_symmetric(K, N, group, packed_w, scales):
     if not h:
         raise QlinError(lib().qlin_last_status(), last_error())
     return h
+
+
+def qlin_quantize(K, N, group, w_ptr, scales_ptr, zeros_ptr, packed_ptr, stream):
+    return lib().qlin_quantize(K, N, group, w_ptr, scales_ptr, zeros_ptr, packed_ptr, stream)
+
+
+def quantize(w, scales, zeros=None, group=128):
+    """Device bf16 weights [N, K] -> device packed codes (torch.int32 view of
+    uint32 words) [N, K/8] on the frozen grid (scales, zeros device bf16
+    [N, K/128]; zeros=None is the symmetric format)."""
+    import torch
+    N, K = w.shape
+    w = w.contiguous()
+    packed = torch.empty((N, K // 8), dtype=torch.int32, device=w.device)
+    zp = zeros.contiguous().data_ptr() if zeros is not None else None
+    _check(qlin_quantize(K, N, group, w.data_ptr(), scales.contiguous().data_ptr(), zp, packed.data_ptr(),
+                         torch.cuda.current_stream().cuda_stream))
+    return packed
 
 
 def qlin_forward(h, M, x_ptr, y_ptr, stream):
@@ -162,12 +186,14 @@ def qlin_shape(h):
 class QLinear:
     """One W4A16 linear layer on the current GPU.
 
-    ``packed``/``scales``/``zeros`` are host arrays in the canonical layout
-    (see include/qlin.h); ``zeros=None`` selects the symmetric format.
+    ``packed``/``scales``/``zeros`` are host arrays or device tensors in the
+    canonical layout (see include/qlin.h); ``zeros=None`` selects the
+    symmetric format.
     """
 
     def __init__(self, packed, scales, zeros=None, group=128):
-        packed = np.asarray(packed)
+        if not hasattr(packed, "data_ptr"):
+            packed = np.asarray(packed)
         self.N, K8 = packed.shape
         self.K = K8 * 8
         if zeros is None:

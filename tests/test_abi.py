@@ -133,3 +133,23 @@ def test_error_state_is_cleared_by_the_next_call(case, monkeypatch):
     assert qlin.qlin_last_status() == qlin.QLIN_ERR_INVALID
     _create_code(256, 32, 128, case["packed"], case["scales"], case["zeros"])
     assert qlin.qlin_last_status() == qlin.QLIN_ERR_OOM
+
+
+def test_quantize_rejects_bad_arguments():
+    """qlin_quantize validates shapes, pointers, alignment and overlap before
+    any HIP call (addresses below are never dereferenced)."""
+    L = qlin.lib()
+    A = 1 << 20                                  # aligned stand-in addresses
+    f = L.qlin_quantize
+    assert f(0, 32, 128, A, A, A, 2 * A, None) == qlin.QLIN_ERR_INVALID
+    assert f(256, 32, 64, A, A, A, 2 * A, None) == qlin.QLIN_ERR_UNSUPPORTED
+    assert f(200, 32, 128, A, A, A, 2 * A, None) == qlin.QLIN_ERR_INVALID
+    assert f(256, 24, 128, A, A, A, 2 * A, None) == qlin.QLIN_ERR_UNSUPPORTED
+    assert f(256, 32, 128, None, A, A, 2 * A, None) == qlin.QLIN_ERR_INVALID
+    assert f(256, 32, 128, A, None, A, 2 * A, None) == qlin.QLIN_ERR_INVALID
+    assert f(256, 32, 128, A, A, A, None, None) == qlin.QLIN_ERR_INVALID
+    assert f(256, 32, 128, A + 8, A, A, 2 * A, None) == qlin.QLIN_ERR_ALIGN
+    assert f(256, 32, 128, A, A, A, 2 * A + 2, None) == qlin.QLIN_ERR_ALIGN
+    assert f(256, 32, 128, A, A + 1, A, 2 * A, None) == qlin.QLIN_ERR_ALIGN
+    assert f(256, 32, 128, A, A, A, A + 256, None) == qlin.QLIN_ERR_INVALID      # packed overlaps w
+    assert "overlaps" in qlin.last_error()

@@ -1,0 +1,109 @@
+"""GPU parity of qlin_quantize (fixed-grid round-to-nearest + packing) with
+the CPU oracle, bit-exact on every packed word (needs an MI355X)."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import qlin_ref as ref
+from paper_2607_04244_amd import qlin
+from synth import gen
+
+pytestmark = pytest.mark.gpu
+
+
+def dev16(a):
+    return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+def host_words(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy().view(np.uint32)
+
+
+def _weights_near_grid(rng, N, K, scales, zeros, spread=0.7):
+    """bf16 weights around the grid points (q - z) s, with exact ties planted:
+    (q - z + 1/2) s is a bf16 value whenever s is a power of two."""
+    s = np.repeat(ref.bf16_to_f64(scales), 128, axis=1)
+    z = np.repeat(ref.bf16_to_f64(zeros), 128, axis=1)
+    q = rng.integers(-2, 18, size=(N, K))                 # a few beyond the clamp
+    off = rng.uniform(-spread, spread, size=(N, K))
+    tie = rng.random((N, K)) < 0.05
+    off[tie] = 0.5 * np.sign(rng.standard_normal(tie.sum()))
+    w = ((q - z) + off) * s
+    return ref.rne_bf16(w.astype(np.float32).astype(np.float64))
+
+
+@pytest.mark.parametrize("symmetric", [False, True])
+@pytest.mark.parametrize("N,K", [(16, 128), (48, 384), (208, 1152), (1024, 2560)])
+def test_quantize_matches_oracle(N, K, symmetric):
+    rng = np.random.default_rng(N + K + symmetric)
+    e = rng.integers(-8, 3, size=(N, K // 128))
+    pow2 = rng.random((N, K // 128)) < 0.5                # power-of-two scales make ties exact
+    sv = np.where(pow2, 2.0 ** e, rng.uniform(0.002, 0.05, size=(N, K // 128)))
+    scales = ref.rne_bf16(sv.astype(np.float32).astype(np.float64))
+    zeros = ref.symmetric_zeros(N, K) if symmetric else ref.rne_bf16(rng.integers(0, 16, size=(N, K // 128)).astype(np.float64))
+    w = _weights_near_grid(rng, N, K, scales, zeros)
+    got = host_words(qlin.quantize(dev16(w), dev16(scales), None if symmetric else dev16(zeros)))
+    assert np.array_equal(got, ref.quantize_pack(w, scales, zeros))
+
+
+def test_quantize_special_values():
+    """Subnormal weights, signed zeros, huge values (clamp) and 0/0 (NaN
+    quotient gives the zero-point)."""
+    N, K = 16, 256
+    w = np.zeros((N, K), np.uint16)
+    w[0, :] = 0x8000                                      # -0
+    w[1, :] = np.arange(K) % 0x7F + 1                     # subnormals
+    w[2, :] = 0x7F00                                      # huge
+    w[3, :] = 0xFF00                                      # -huge
+    w[4, :] = 0x0001                                      # smallest subnormal
+    scales = np.full((N, K // 128), 0x3F80, np.uint16)
+    scales[1, :] = 0x0080                                 # 2^-126: subnormal w / s is O(1)
+    scales[4, :] = 0x0000                                 # 0 -> w / 0 = inf, and row 5 below 0 / 0 = NaN
+    scales[5, :] = 0x0000
+    zeros = ref.rne_bf16(np.full((N, K // 128), 6.0))
+    got = host_words(qlin.quantize(dev16(w), dev16(scales), dev16(zeros)))
+    assert np.array_equal(got, ref.quantize_pack(w, scales, zeros))
+
+
+def test_quantize_inverts_the_handles_dequantization():
+    """Round trip on the device: the bf16 weights the handle dequantizes are
+    quantized back to the very codes it was built from (config-1 shape)."""
+    c = gen.linear_case(1)
+    lin = qlin.QLinear(c["packed"], c["scales"], c["zeros"])
+    w = lin.dequantize(0)
+    got = host_words(qlin.quantize(w, dev16(c["scales"]), dev16(c["zeros"])))
+    assert np.array_equal(got, c["packed"])
+    lin.close()
+
+
+def test_handle_from_device_quantized_weights():
+    """Quantize on the device, build the handle from the device arrays, and
+    run the layer: equals the oracle on the same codes."""
+    rng = np.random.default_rng(3)
+    N, K, M = 256, 1280, 16
+    c = gen.random_case(3, M, K, N)
+    w = _weights_near_grid(rng, N, K, c["scales"], c["zeros"])
+    s_d, z_d = dev16(c["scales"]), dev16(c["zeros"])
+    packed_d = qlin.quantize(dev16(w), s_d, z_d)
+    lin = qlin.QLinear(packed_d, s_d, z_d)
+    packed = ref.quantize_pack(w, c["scales"], c["zeros"])
+    y = lin.forward(dev16(c["x"]))
+    torch.cuda.synchronize()
+    r = ref.compare(y.view(torch.int16).cpu().numpy().view(np.uint16),
+                    ref.forward(c["x"], packed, c["scales"], c["zeros"]))
+    assert r["ok"], r
+    lin.close()
+
+
+def test_quantize_argument_errors_on_device():
+    w = torch.zeros((32, 256), dtype=torch.bfloat16, device="cuda")
+    s = torch.ones((32, 2), dtype=torch.bfloat16, device="cuda")
+    out = torch.empty((32, 32), dtype=torch.int32, device="cuda")
+    f = qlin.qlin_quantize
+    assert f(256, 32, 128, w.data_ptr() + 2, s.data_ptr(), None, out.data_ptr(), None) == qlin.QLIN_ERR_ALIGN
+    assert f(256, 32, 128, w.data_ptr(), s.data_ptr(), None, w.data_ptr(), None) == qlin.QLIN_ERR_INVALID
+    assert f(256, 32, 128, w.data_ptr(), s.data_ptr(), None, out.data_ptr(), None) == qlin.QLIN_OK
+    torch.cuda.synchronize()
+    assert torch.all(out.view(torch.int32) == np.int32(np.uint32(0x88888888).view(np.int32)))
