@@ -7,6 +7,9 @@
 
 namespace qlin {
 
+typedef __attribute__((address_space(3))) void lds_void_t;   // LDS, for direct-to-LDS loads
+typedef __attribute__((address_space(1))) void glb_void_t;   // global memory
+
 typedef short v4s __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v2f __attribute__((ext_vector_type(2)));
@@ -67,31 +70,51 @@ __device__ inline Pairs extract_pairs(uint32_t P, const ExtractConsts &k) {
 // One lane's 16 bytes of a weight block.
 __device__ inline uint4 load_block(const uint4 *codes, size_t idx) { return codes[idx]; }
 
-// s | z << 16 word of a column (symmetric handles store only s; z = 8).
+// Per (column, group) dequantization word: bf16 s in the low half and the
+// bf16 offset zc = -(128 + z) in the high half (exact: an integer of 8
+// significant bits), so that (128 + q) * s + zc * s = (q - z) * s.
+// Symmetric handles store only s (z = 8, zc = -136 = bf16 0xC308).
+constexpr uint32_t kZcSymmetric = 0xC308u;
 template <bool SYM>
 __device__ inline uint32_t load_sz(const void *sz, size_t idx) {
     if constexpr (SYM) {
-        return (uint32_t)((const uint16_t *)sz)[idx] | (0x4100u << 16);
+        return (uint32_t)((const uint16_t *)sz)[idx] | (kZcSymmetric << 16);
     } else {
         return ((const uint32_t *)sz)[idx];
     }
 }
 
+__device__ inline float dot2(uint32_t a, uint32_t b, float c) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(v2bf, a), __builtin_bit_cast(v2bf, b), c, false);
+}
+
+// c = s * zc of a dequantization word, exactly (one bf16 product, plus 0)
+__device__ inline float sz_offset(uint32_t sz) { return dot2(sz, sz >> 16, 0.0f); }
+
 // --- matrix-core dequantization ------------------------------------------
 
 struct MfmaDeq { v4s bdiag; v4f c4; };
 
+// Byte selectors (v_perm_b32) that place the bf16 s of a dequantization
+// word into element l & 3 of lane l's B operand (two dwords, four bf16) and
+// zero the other three elements.  Constant per lane; built once per kernel.
+struct DiagSel {
+    uint32_t s0, s1;
+    __device__ inline explicit DiagSel(int lane) {
+        constexpr uint32_t kLo = 0x0C0C0100u, kHi = 0x01000C0Cu, kZero = 0x0C0C0C0Cu;
+        const int r = lane & 3;
+        s0 = r == 0 ? kLo : r == 1 ? kHi : kZero;
+        s1 = r == 2 ? kLo : r == 3 ? kHi : kZero;
+    }
+};
+
 // Per-group constants of lane l for column n = 16 t + (l & 15):
 // B = diag(s) in the 4x4 block layout (this lane supplies B[r][l & 3],
-// non-zero only for r = l & 3) and C = -(128 + z) * s in all four rows.
-__device__ inline MfmaDeq mfma_setup(uint32_t sz, uint32_t shift, uint32_t keep_lo) {
-    const float s = bf16_lo_to_f32(sz);
-    const float z = bf16_hi_to_f32(sz);
-    const float c = -((z + 128.0f) * s);
-    const uint32_t v = (sz & 0xFFFFu) << shift;     // s in half (l & 1)
-    const uint32_t b0 = v & keep_lo, b1 = v & ~keep_lo;
+// non-zero only for r = l & 3) and C = zc * s = -(128 + z) * s in all four rows.
+__device__ inline MfmaDeq mfma_setup(uint32_t sz, const DiagSel &sel) {
+    const float c = sz_offset(sz);
     MfmaDeq d;
-    d.bdiag = __builtin_bit_cast(v4s, v2u{b0, b1});
+    d.bdiag = __builtin_bit_cast(v4s, v2u{__builtin_amdgcn_perm(sz, sz, sel.s0), __builtin_amdgcn_perm(sz, sz, sel.s1)});
     d.c4 = v4f{c, c, c, c};
     return d;
 }
@@ -119,17 +142,11 @@ __device__ inline ValuDeq valu_setup(const uint32_t sz[4]) {
     ValuDeq d;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        const float s = bf16_lo_to_f32(sz[r]);
-        const float z = bf16_hi_to_f32(sz[r]);
-        d.c[r] = -((z + 128.0f) * s);
+        d.c[r] = sz_offset(sz[r]);   // -(128 + z) * s
         d.sl[r] = sz[r] & 0xFFFFu;   // bf16 pair (s, 0)
         d.sh[r] = sz[r] << 16;       // bf16 pair (0, s)
     }
     return d;
-}
-
-__device__ inline float dot2(uint32_t a, uint32_t b, float c) {
-    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(v2bf, a), __builtin_bit_cast(v2bf, b), c, false);
 }
 
 // Dequantize one packed word: pr[r] = bf16 pair (w[n_r][k0], w[n_r][k0 + 4]) with

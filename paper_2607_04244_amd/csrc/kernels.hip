@@ -75,7 +75,9 @@ __global__ void k_repack_sz(const uint16_t *__restrict__ scales, const uint16_t 
         if (symmetric) {
             ((uint16_t *)out)[idx] = s;
         } else {
-            ((uint32_t *)out)[idx] = (uint32_t)s | ((uint32_t)zeros[n * Kb + kb] << 16);
+            // zc = -(128 + z): bf16 sign 1, exponent of 128, mantissa z (z integer in [0, 15])
+            const uint32_t z = (uint32_t)__uint_as_float((uint32_t)zeros[n * Kb + kb] << 16);
+            ((uint32_t *)out)[idx] = (uint32_t)s | ((0xC300u | z) << 16);
         }
     }
 }
@@ -106,12 +108,12 @@ __global__ void k_dequant_mfma(const uint4 *__restrict__ codes, const void *__re
     const int Kb = K / kGroup;
     const size_t nblocks = (size_t)(N / kTileN) * Kb;
     const int l = threadIdx.x & 63;
-    const uint32_t shift = (l & 1) * 16, keep_lo = (l & 2) ? 0u : 0xFFFFFFFFu;
+    const DiagSel dsel(l);
     const ExtractConsts kx;
     for (size_t b = (size_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); b < nblocks;
          b += (size_t)gridDim.x * (blockDim.x >> 6)) {
         const uint4 c = codes[b * 64 + l];
-        const MfmaDeq d = mfma_setup(load_sz<SYM>(sz, b * kTileN + (l & 15)), shift, keep_lo);
+        const MfmaDeq d = mfma_setup(load_sz<SYM>(sz, b * kTileN + (l & 15)), dsel);
         const uint32_t P[4] = {c.x, c.y, c.z, c.w};
         const int t = (int)(b / Kb), kb = (int)(b % Kb);
         const size_t n = (size_t)t * kTileN + (l & 15);
@@ -321,7 +323,18 @@ __device__ inline void write_out(const FwdArgs &a, const WgWork &w, const float 
     if (!direct) reduce_chunks(a, w);
 }
 
-constexpr int kStageMax = (kXChunksMax + kThreads - 1) / kThreads;
+// One direct-to-LDS 16-byte load per lane: lane l's 16 bytes from src land
+// at lds_dst + 16 l (lds_dst uniform across the wave).  Issued as inline
+// assembly so that the compiler does not track it: its wait-count pass
+// handles direct-to-LDS writes coarsely and would drain every outstanding
+// load before each later LDS read.  The caller waits for it explicitly
+// (s_waitcnt vmcnt) before the barrier that publishes the data; loads the
+// compiler does track and issues later are younger, so its own waits stay
+// sufficient.
+__device__ inline void load_lds_x16(const void *src, const uint4 *lds_dst) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds_dst);
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" :: "s"(m0), "v"(src) : "memory", "m0");
+}
 
 // Barrier for LDS hand-off only.  __syncthreads() also waits for every
 // outstanding global load, which would drain the weight prefetch.
@@ -329,43 +342,28 @@ __device__ inline void lds_barrier() {
     asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// x chunks staged per thread: the planner never gives a workgroup more than
-// kXChunksMax 16-byte chunks, so one unrolled batch per thread covers them.
-// The chunk sequence idx = bb * kThreads + tid is walked as (row m, chunk q8)
-// with increments only.
-struct StageWalk {
-    int m, q8, dm, dq;
-    __device__ inline void start(int n8, int tid) {
-        dm = kThreads / n8;
-        dq = kThreads - dm * n8;
-        m = tid / n8;                 // once per thread
-        q8 = tid - m * n8;
-    }
-    __device__ inline void next(int n8) {
-        m += dm;
-        q8 += dq;
-        if (q8 >= n8) { q8 -= n8; ++m; }
-    }
-};
-
 // ---- SKINNY: matrix-core dequantization + v_mfma_f32_16x16x32_bf16 --------
 //
 // A workgroup owns K chunk c (groups [g0, g0 + Kc)) of column tiles
 // [t0, t0 + Tn).  It stages x[:, chunk] in LDS once, in MFMA B-operand order,
-// while its first weight blocks are already in flight; its waves then split
-// the Tn * Kc blocks evenly (tile-major order), each keeping kDepth 1 KiB
-// blocks in flight.  A wave leaves one partial sum per tile it touches in an
-// LDS slot; write_out() adds them in a fixed order.
+// with direct-to-LDS loads (global_load_lds_dwordx4: no VGPR round trip, no
+// LDS write instructions) while its first weight blocks are already in
+// flight; its waves then split the Tn * Kc blocks evenly (tile-major order),
+// each keeping kDepth 1 KiB blocks in flight.  A wave leaves one partial sum
+// per tile it touches in an LDS slot; write_out() adds them in a fixed order.
 //
-// x in LDS: 16-byte fragments, fragment (kbl, c, row) = x[row][k0 .. k0 + 8)
-// with k0 = 128(g0 + kbl) + 8c, c = 4j + g < 16, for rows < M only, stored
-// at slot (16 kbl + c) * XR + (row & ~msk) + ((row ^ c) & msk), where XR =
-// staged_rows(M) (1, 2, 4, 8, 16 or 16 * MT) and msk = min(XR, 16) - 1.  The
-// XOR swizzle keeps both the staging writes (16 lanes = 16 consecutive c of
-// one row) and the operand reads (16 lanes = 16 rows of one c) on distinct
-// LDS banks.  Lane l of m-tile mt reads c = 4j + (l >> 4) of row
-// min(16 mt + (l & 15), M - 1).
-template <int MT, bool SYM>
+// x in LDS: 16-byte fragments, fragment (row, q8) = x[row][k0 .. k0 + 8)
+// with k0 = 128 g0 + 8 q8 (q8 = 16 kbl + c, c = 4j + g < 16), row-major at
+// slot row * (n8 + 1) + q8, n8 = 16 Kc: each row is the chunk's 256 Kc
+// contiguous bytes plus one 16-byte pad slot.  A direct-to-LDS load fills 64
+// consecutive slots = one contiguous KiB of a row of x (coalesced); the pad
+// shifts consecutive rows by 4 banks, so the operand reads (16 lanes = 16
+// rows of one q8) hit distinct banks; and a lane's four reads of a block are
+// one address plus immediate offsets (4 j slots).  XR = staged rows (the
+// next power of two >= M for one m-tile, else 16 MT).  Lane l of m-tile mt
+// reads row min(16 mt + (l & 15), M - 1); pad slots and rows >= M hold
+// copies and are never read.
+template <int MT, int XR, bool SYM>
 __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     extern __shared__ __align__(16) unsigned char smem[];
     constexpr int MR = 16 * MT;
@@ -373,34 +371,26 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform: keeps the walk on the scalar unit
     const ExtractConsts kx;
     const WgWork w = wg_work(a, blockIdx.x);
-    // staged rows: next power of two >= M for one m-tile, else MR
-    int XR = MR;
-    if (MT == 1) { XR = 1; while (XR < a.M) XR <<= 1; }
-    const int msk = min(XR, 16) - 1;
     uint4 *xs = (uint4 *)smem;
-    float *slots = (float *)(smem + (size_t)w.Kc * XR * 256);
+    const int n8 = w.Kc * 16;                         // 16-byte chunks per row of the x chunk
+    const int nslots = XR * (n8 + 1);
+    const int nload = (nslots + 63) >> 6;             // direct-to-LDS loads of the workgroup
+    float *slots = (float *)(smem + (size_t)nload * 1024);
 
     const int U = w.Tn * w.Kc;
     int u0, u1;
     wave_range(U, wave, u0, u1);
     const int lm = lane & 15, lg = lane >> 4;
-    const uint32_t shift = (lane & 1) * 16, keep_lo = (lane & 2) ? 0u : 0xFFFFFFFFu;
+    const DiagSel dsel(lane);
 
-    // 1) issue the x loads of the whole chunk, rows < M only
-    const int n8 = w.Kc * 16;
-    const int total = min(a.M, MR) * n8;
-    uint4 v[kStageMax];
-    {
-        StageWalk sw;
-        sw.start(n8, tid);
-#pragma unroll
-        for (int bb = 0; bb < kStageMax; ++bb) {
-            v[bb] = make_uint4(0, 0, 0, 0);
-            if (bb * kThreads + tid < total)
-                v[bb] = *(const uint4 *)(a.x + (size_t)sw.m * a.K + (size_t)(w.g0 + (sw.q8 >> 4)) * kGroup +
-                                         (sw.q8 & 15) * 8);
-            sw.next(n8);
-        }
+    // 1) the x chunk, straight into LDS: load i fills slots [64 i, 64 i + 64)
+    //    (the last one may run past the chunk into spare LDS)
+    for (int i = wave; i < nload; i += kWaves) {
+        const int sl = i * 64 + lane;
+        const int r = sl / (n8 + 1);                  // row; q8 == n8 is the pad slot
+        const int q8 = min(sl - r * (n8 + 1), n8 - 1);
+        const int row = min(r, a.M - 1);
+        load_lds_x16(a.x + (size_t)row * a.K + (size_t)w.g0 * kGroup + q8 * 8, xs + i * 64);
     }
     // 2) then the first weight blocks (younger than the x loads, so waiting
     //    for x below does not wait for them).  A wave with an empty range
@@ -416,30 +406,16 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
         sb[d] = load_sz<SYM>(a.sz, pw.b * kTileN + lm);
         if (up + 1 < u1) { pw.next(w, a.Kb); ++up; }
     }
-    // 3) write x to LDS in fragment order
-    {
-        StageWalk sw;
-        sw.start(n8, tid);
-#pragma unroll
-        for (int bb = 0; bb < kStageMax; ++bb) {
-            if (bb * kThreads + tid < total) {
-                const int c = sw.q8 & 15;          // (kbl, c) with kbl = q8 >> 4
-                xs[sw.q8 * XR + (sw.m & ~msk) + ((sw.m ^ c) & msk)] = v[bb];
-            }
-            sw.next(n8);
-        }
-    }
+    // 3) every wave's x loads have landed in LDS (only the weight prefetch,
+    //    2 kDepth loads, may still be in flight)
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * kDepth) : "memory");
     lds_barrier();
 
-    // LDS row read by lane row lm of m-tile mt: rows >= M (never staged) read
-    // row M - 1; they only feed output columns >= M, which are not written
-    int xoff[MT][4];           // (row & ~msk) + ((row ^ c) & msk) for c = 4j + lg
+    // per-lane part of the operand read slot: q8 = 16 kbl + 4 j + lg, so the
+    // slot is 16 kbl + 4 j + xoff[mt]
+    int xoff[MT];
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int r = min(16 * mt + lm, a.M - 1);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) xoff[mt][j] = (r & ~msk) + ((r ^ (4 * j + lg)) & msk);
-    }
+    for (int mt = 0; mt < MT; ++mt) xoff[mt] = min(16 * mt + lm, a.M - 1) * (n8 + 1) + lg;
 
     if (u0 < u1) {
         v4f acc[MT];
@@ -451,11 +427,12 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
         auto consume = [&](int u, const uint4 &cq, uint32_t szw) {
             v8bf xf[MT][4];
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
+            for (int mt = 0; mt < MT; ++mt) {
+                const uint4 *xb = xs + cw.kbl * 16 + xoff[mt];
 #pragma unroll
-                for (int mt = 0; mt < MT; ++mt)
-                    xf[mt][j] = __builtin_bit_cast(v8bf, xs[(cw.kbl * 16 + 4 * j + lg) * XR + xoff[mt][j]]);
-            const MfmaDeq d = mfma_setup(szw, shift, keep_lo);
+                for (int j = 0; j < 4; ++j) xf[mt][j] = __builtin_bit_cast(v8bf, xb[4 * j]);
+            }
+            const MfmaDeq d = mfma_setup(szw, dsel);
             const uint32_t P[4] = {cq.x, cq.y, cq.z, cq.w};
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -615,7 +592,7 @@ __global__ void __launch_bounds__(kThreads) k_mfma16(FwdArgs a) {
     int u0, u1;
     wave_range(Tn * w.Kc, wave, u0, u1);
     const int lm = lane & 15, lg = lane >> 4;
-    const uint32_t shift = (lane & 1) * 16, keep_lo = (lane & 2) ? 0u : 0xFFFFFFFFu;
+    const DiagSel dsel(lane);
 
     v4f acc[TN];
 #pragma unroll
@@ -641,7 +618,7 @@ __global__ void __launch_bounds__(kThreads) k_mfma16(FwdArgs a) {
 #pragma unroll
             for (int t = 0; t < TN; ++t) {
                 if (t >= ta && t < tb) {
-                    const MfmaDeq d = mfma_setup(B.s[t], shift, keep_lo);
+                    const MfmaDeq d = mfma_setup(B.s[t], dsel);
                     const uint32_t P[4] = {B.c[t].x, B.c[t].y, B.c[t].z, B.c[t].w};
 #pragma unroll
                     for (int j = 0; j < 4; ++j)
@@ -707,8 +684,8 @@ __global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
                 B.c[t] = load_block(a.codes, b * 64 + lane);
                 if constexpr (SYM) {
                     const uint2 h = *(const uint2 *)((const uint16_t *)a.sz + b * kTileN + 4 * b2);
-                    B.s[t] = make_uint4((h.x & 0xFFFFu) | (0x4100u << 16), (h.x >> 16) | (0x4100u << 16),
-                                        (h.y & 0xFFFFu) | (0x4100u << 16), (h.y >> 16) | (0x4100u << 16));
+                    B.s[t] = make_uint4((h.x & 0xFFFFu) | (kZcSymmetric << 16), (h.x >> 16) | (kZcSymmetric << 16),
+                                        (h.y & 0xFFFFu) | (kZcSymmetric << 16), (h.y >> 16) | (kZcSymmetric << 16));
                 } else {
                     B.s[t] = *(const uint4 *)((const uint32_t *)a.sz + b * kTileN + 4 * b2);
                 }
@@ -904,12 +881,16 @@ static FwdKernel pick_regs(int kern, int mrows) {
 
 template <bool SYM>
 static FwdKernel pick(int kern, int mrows, int tn) {
-    if (kern == kKernStaged) {
-        switch (mrows) {
-            case 16: return k_skinny<1, SYM>;
-            case 32: return k_skinny<2, SYM>;
-            case 48: return k_skinny<3, SYM>;
-            case 64: return k_skinny<4, SYM>;
+    if (kern == kKernStaged) {        // tn = staged rows XR
+        switch (tn) {
+            case 1: return k_skinny<1, 1, SYM>;
+            case 2: return k_skinny<1, 2, SYM>;
+            case 4: return k_skinny<1, 4, SYM>;
+            case 8: return k_skinny<1, 8, SYM>;
+            case 16: return k_skinny<1, 16, SYM>;
+            case 32: return k_skinny<2, 32, SYM>;
+            case 48: return k_skinny<3, 48, SYM>;
+            case 64: return k_skinny<4, 64, SYM>;
         }
         return nullptr;
     }
@@ -935,7 +916,7 @@ const char *kernel_name(int kern, int mrows, int tn, bool symmetric) {
     if (kern == kKernTiled) snprintf(buf, sizeof buf, "k_tiled%s", symmetric ? "<sym>" : "");
     else if (kern == kKernMfma16) snprintf(buf, sizeof buf, "k_mfma16<%d%s>", tn, symmetric ? ",sym" : "");
     else if (kern == kKernGemv) snprintf(buf, sizeof buf, "k_gemv4<%d,%d%s>", mrows, tn, symmetric ? ",sym" : "");
-    else snprintf(buf, sizeof buf, "k_skinny<%d%s>", mrows / 16, symmetric ? ",sym" : "");
+    else snprintf(buf, sizeof buf, "k_skinny<%d,%d%s>", mrows / 16, tn, symmetric ? ",sym" : "");
     return buf;
 }
 
@@ -948,8 +929,8 @@ hipError_t prepare_kernels() {
                 (void)hipFuncSetAttribute((const void *)pick_kernel(kKernGemv, mv, tn, sym),
                                           hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
         }
-        for (int mr = 16; mr <= 64; mr += 16)
-            (void)hipFuncSetAttribute((const void *)pick_kernel(kKernStaged, mr, 0, sym),
+        for (int xr : {1, 2, 4, 8, 16, 32, 48, 64})
+            (void)hipFuncSetAttribute((const void *)pick_kernel(kKernStaged, 0, xr, sym),
                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLdsMax);
     }
     return hipSuccess;

@@ -120,9 +120,7 @@ int check_zeros(const uint16_t *z, size_t n) {
 
 // Does a K chunk of Kc groups fit one SKINNY workgroup with M rows (staged x
 // + one column tile)?
-bool chunk_fits(int M, int Kc) {
-    return x_chunks(M, Kc) <= kXChunksMax && lds_bytes(M, Kc, 1) <= kLdsMax;
-}
+bool chunk_fits(int M, int Kc) { return lds_bytes(M, Kc, 1) <= kLdsMax; }
 
 // Smallest number of K chunks whose chunks fit a SKINNY workgroup.
 int min_split(int M, int Kb) {
@@ -237,7 +235,7 @@ struct Plan {
     int kern = 0;
     int mrows = 0;     // template row count (GEMV: M; MFMA kernels: 16 * m-tiles)
     int S = 1, Gn = 1, grid = 1;
-    int tn = 0;        // tile slots of the register-resident kernels: max tiles per range
+    int tn = 0;        // REGS/GEMV: tile slots (max tiles per range); SKINNY: staged x rows
     size_t lds = 0;
 };
 
@@ -369,7 +367,7 @@ int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
     p->grid = bestS * bestGn;
     const bool regs = bestK != kKernStaged;
     const int Kc = (h->Kb + bestS - 1) / bestS, Tn = (h->Nt + bestGn - 1) / bestGn;
-    p->tn = regs ? Tn : 0;
+    p->tn = regs ? Tn : bestK == kKernStaged ? staged_rows(Mi) : 0;
     const size_t need = regs ? lds_bytes_regs(p->mrows, Tn) : lds_bytes(Mi, Kc, Tn);
     // at least 80 KiB + 1 of LDS per workgroup keeps one workgroup per CU, so
     // the grid spreads over all CUs

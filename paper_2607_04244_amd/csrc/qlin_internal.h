@@ -25,7 +25,6 @@ constexpr int kMaxGemvM = 4;
 constexpr int kTnMax = 8;          // column tiles per workgroup, register-resident kernels
 constexpr int kTnMaxGemv = 4;      // the same for the vector-ALU GEMV kernel
 constexpr size_t kLdsMax = 160 * 1024 - 512;   // dynamic LDS per workgroup (static use is tiny)
-constexpr int kXChunksMax = 8192;  // 16-byte x chunks one workgroup stages (128 KiB)
 
 enum Path { kAuto = 0, kGemv = 1, kSkinny = 2, kTiled = 3, kRegs = 4 };
 
@@ -44,7 +43,7 @@ enum Kern {
 // division to find their work.
 struct FwdArgs {
     const uint4 *codes;     // device layout, Nt * Kb blocks of 1 KiB
-    const void *sz;         // per (tile, group, column): u32 s | z << 16, or u16 s (symmetric)
+    const void *sz;         // per (tile, group, column): u32 s | zc << 16 with zc = -(128 + z), or u16 s (symmetric)
     const uint16_t *x;      // [M][K] bf16
     uint16_t *y;            // [M][N] bf16
     float *ws;              // fp32 partial sums (S > 1): S * Gn regions of TnMax * M * 16
@@ -86,20 +85,20 @@ inline int staged_rows(int M) {
     return r;
 }
 
-// 16-byte x chunks a SKINNY workgroup loads for a K chunk of Kc groups.
-inline int x_chunks(int M, int Kc) { return M * Kc * 16; }
-
 // LDS bytes of the register-resident kernels with tn tile slots: one slot of
 // rows x 16 fp32 per (wave, tile).
 inline size_t lds_bytes_regs(int rows, int tn) { return (size_t)kWaves * tn * rows * 16 * 4; }
 
 // LDS bytes of a SKINNY workgroup with M rows: the x chunk of Kc groups
-// (staged_rows(M) rows) plus one partial-sum slot (16 m-columns per m-tile x
-// 16 fp32) per (wave, column tile) pair a wave touches; slot = wave + tile is
-// unique, so kWaves + Tn - 1 slots suffice.
+// (staged_rows(M) rows of 16 Kc + 1 slots of 16 bytes, in whole 1 KiB
+// direct-to-LDS loads) plus one
+// partial-sum slot (16 m-columns per m-tile x 16 fp32) per (wave, column
+// tile) pair a wave touches; slot = wave + tile is unique, so kWaves + Tn - 1
+// slots suffice.
 inline size_t lds_bytes(int M, int Kc, int Tn) {
     const int mrows = 16 * ((M + 15) / 16);
-    return (size_t)Kc * staged_rows(M) * 256 + (size_t)(kWaves + Tn) * mrows * 16 * 4;
+    const size_t x = ((size_t)staged_rows(M) * (Kc * 16 + 1) * 16 + 1023) / 1024 * 1024;
+    return x + (size_t)(kWaves + Tn) * mrows * 16 * 4;
 }
 
 // Host launchers (kernels.hip).  Each returns the launch status.

@@ -36,8 +36,6 @@ namespace qlin {
 // the column block's weights are fetched once into that XCD's L2 and reused
 // by the row blocks.  Rows >= M and tiles >= Nt load a clamped valid row or
 // tile and are not written.
-typedef __attribute__((address_space(3))) void lds_void_t;
-typedef __attribute__((address_space(1))) void glb_void_t;
 
 template <bool SYM>
 __global__ void __launch_bounds__(kTiledWaves * 64, 2) k_tiled(TiledArgs a) {
@@ -59,7 +57,7 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 2) k_tiled(TiledArgs a) {
     const int jn = jg * 8 + xcd;
     if (jn >= a.Gn) return;                           // uniform: padding of the grid
     const int lm = lane & 15, lg = lane >> 4;
-    const uint32_t shift = (lane & 1) * 16, keep_lo = (lane & 2) ? 0u : 0xFFFFFFFFu;
+    const DiagSel dsel(lane);
 
     // x: load i of wave w fills rows 16 w + 4 i + (lane >> 4), slot position
     // lane & 15, which holds chunk (lane & 15) ^ (row & 15) of that row.
@@ -111,7 +109,7 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 2) k_tiled(TiledArgs a) {
             cw[t] = ws_codes[buf][slot + lane];
             if constexpr (SYM) {
                 const uint32_t pair = ws_sz[buf][slot + (lm >> 1)];
-                sw[t] = ((lm & 1) ? (pair >> 16) : (pair & 0xFFFFu)) | (0x4100u << 16);
+                sw[t] = ((lm & 1) ? (pair >> 16) : (pair & 0xFFFFu)) | (kZcSymmetric << 16);
             } else {
                 sw[t] = ws_sz[buf][slot + lm];
             }
@@ -133,7 +131,7 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 2) k_tiled(TiledArgs a) {
         read_w(buf, cw, sw);
         MfmaDeq d[kTiledNT];
 #pragma unroll
-        for (int t = 0; t < kTiledNT; ++t) d[t] = mfma_setup(sw[t], shift, keep_lo);
+        for (int t = 0; t < kTiledNT; ++t) d[t] = mfma_setup(sw[t], dsel);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             v8bf wa[kTiledNT];
