@@ -48,10 +48,17 @@ def algorithmic_bytes(M, K, N, symmetric=False):
     return K * N // 2 + per_group * (K // 128) * N + 2 * M * K + 2 * M * N
 
 
-def file_hash(path):
+def device_sources_hash():
+    """sha256 (16 hex digits) of every device source of the library, in name
+    order: identifies the kernels a stored counter summary was taken on."""
     import hashlib
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    d = os.path.join(ROOT, "paper_2607_04244_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(d)):
+        if name.endswith((".hip", ".h")):
+            with open(os.path.join(d, name), "rb") as f:
+                h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
 
 
 def traffic_from_profiles(kernel_src_hash, kernel):
@@ -62,7 +69,7 @@ def traffic_from_profiles(kernel_src_hash, kernel):
         t = json.load(open(p))
     except (OSError, ValueError):
         return None
-    if t.get("kernels_hip_sha256_16") != kernel_src_hash:
+    if t.get("device_sources_sha256_16") != kernel_src_hash:
         return None
     e = t.get("kernels", {}).get(kernel)
     return None if e is None else e.get("hbm_bytes_per_launch")
@@ -316,7 +323,7 @@ def main():
     ceil_gbs, ceil_us = stream_read_ceiling(torch, qlin, bytes_step, stream)
 
     kernel = plan.split("kernel=")[1].split()[0] if "kernel=" in plan else "?"
-    src_hash = file_hash(os.path.join(ROOT, "paper_2607_04244_amd", "csrc", "kernels.hip"))
+    src_hash = device_sources_hash()
     traffic = traffic_from_profiles(src_hash, kernel)
     wl = {"verify": "draft-block verification linear: M=16, K=2560, N=19456 (fused gate+up)"}.get(
         args.workload, f"{args.workload}: M={M}, K={K}, N={N}")
