@@ -22,7 +22,11 @@ Other modes (not the benchmark line): ``--workload`` c0 | c2m1 | c2m4 |
 c2m8 | c2m16 | model (36 layers x 6 linears at M=16, microseconds per
 verification step) | prefill128 | prefill512 | prefill2048 (the same linears
 at M rows, TFLOP/s and matrix-core utilisation) | quantize (bf16 -> packed
-int4 codes on a fixed grid, GB/s); ``--fuse-qkv`` runs the
+int4 codes on a fixed grid, GB/s) | swa1024 | swa2048 | attn-full |
+attn-short (the drafter's block attention: 32 query heads over 8 key/value
+heads of dimension 128, 16 block queries, a T = 8192 cache with a symmetric
+window of 1024 or 2048 tokens, full attention, and T = 700 inside the
+window; GB/s of the visible key/value span); ``--fuse-qkv`` runs the
 q, k, v projections of a layer as one launch; ``--calibrate-copy`` runs a
 plain 256 MiB device copy for the HBM-traffic counter calibration.
 """
@@ -226,6 +230,66 @@ def bench_quantize(args):
                       "pct_of_peak_hbm": round(100 * nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 2)}), flush=True)
 
 
+ATTN_WORKLOADS = {"swa1024": "swa1024", "swa2048": "swa2048", "attn-full": "full", "attn-short": "short"}
+
+
+def attn_span(T, nq, window):
+    """Keys [lo, T) some block query can see (the window or the fallback)."""
+    if window == 0 or T <= window:
+        return 0, T
+    return max(0, T - nq - window // 2), T
+
+
+def bench_attention(args, name):
+    """Drafter block attention: one qlin_swa_attention call per step over
+    rotating copies of the key/value cache (> 1 GiB together, so the reads
+    come from HBM, not the last-level cache), replayed from a HIP graph.
+    Algorithmic bytes: the visible key/value span, q and the output."""
+    import torch
+
+    from oracle import attn_ref as ar
+    from paper_2607_04244_amd import qlin
+    from synth import gen
+    torch.cuda.set_device(0)
+    c = gen.attention_case(ATTN_WORKLOADS[name])
+    Hq, Hkv, nq, T, W = c["Hq"], c["Hkv"], c["nq"], c["T"], c["window"]
+    lo, hi = attn_span(T, nq, W)
+    nbytes = Hkv * (hi - lo) * 128 * 2 * 2 + 2 * Hq * nq * 128 * 2
+    dev = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    q = dev(c["q"])
+    k0, v0 = dev(c["k"]), dev(c["v"])
+    cache_bytes = 2 * k0.numel() * 2
+    R = max(2, -(-(1 << 30) // cache_bytes))
+    kvs = [(k0, v0)] + [(k0.clone(), v0.clone()) for _ in range(R - 1)]
+    S, ws_bytes, plan = qlin.qlin_swa_plan(Hq, Hkv, 128, nq, T, W, args.split)
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
+    out = torch.empty((Hq, nq, 128), dtype=torch.bfloat16, device="cuda")
+    stream = torch.cuda.Stream()
+    calls = [(lambda k=k, v=v: qlin.swa_attention(q, k, v, W, splits=args.split, out=out, workspace=ws))
+             for k, v in kvs]
+    with torch.cuda.stream(stream):
+        for i in range(args.warmup):
+            calls[i % R]()
+    stream.synchronize()
+    us, _ = graph_time_us(torch, stream, calls, reps=max(2, args.steps // R))
+    gbs = nbytes / (us * 1e-6) / 1e9
+    res = {"workload": f"drafter block attention {name}: Hq={Hq}, Hkv={Hkv}, d=128, nq={nq}, T={T}, "
+                       f"window={W or 'full'} ({hi - lo} visible keys per head, {R} rotating caches)",
+           "us_per_call": round(us, 3), "bytes_per_call": nbytes, "GBps": round(gbs, 1),
+           "pct_of_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2), "plan": plan}
+    if not args.no_cpu:
+        times = []
+        t_start = time.perf_counter()
+        while time.perf_counter() - t_start < 10.0 and len(times) < 20:
+            t0 = time.perf_counter()
+            ar.swa_attention(c["q"], c["k"], c["v"], W)
+            times.append(time.perf_counter() - t0)
+        t = float(np.median(times))
+        res["cpu_baseline"] = {"value": round(nbytes / t / 1e9, 4), "unit": "GB/s", "kind": "oracle",
+                               "sample": f"{len(times)} whole oracle calls (median {t:.3f} s)"}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -251,6 +315,8 @@ def main():
         return bench_model(args, fuse_qkv=args.fuse_qkv)
     if args.workload == "quantize":
         return bench_quantize(args)
+    if args.workload in ATTN_WORKLOADS:
+        return bench_attention(args, args.workload)
 
     import torch
 

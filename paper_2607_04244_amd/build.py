@@ -11,9 +11,11 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libqlin.so")
-# (source, extra flags).  tiled.hip keeps matrix-core results in VGPRs: its
-# dequantizing 4x4x4 products feed vector instructions directly.
-SOURCES = [("kernels.hip", []), ("tiled.hip", ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]), ("qlin.cpp", [])]
+# (source, extra flags).  tiled.hip and attn.hip keep matrix-core results in
+# VGPRs: their products feed vector instructions directly (dequantization,
+# softmax rescaling), which would otherwise go through AGPR copies.
+SOURCES = [("kernels.hip", []), ("tiled.hip", ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]), ("attn.hip", ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]),
+           ("qlin.cpp", []), ("attn_abi.cpp", [])]
 ARCH = "gfx950"
 
 # Packed-fp32 vector instructions are switched off in the device pass; the

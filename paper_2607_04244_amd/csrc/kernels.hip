@@ -323,25 +323,6 @@ __device__ inline void write_out(const FwdArgs &a, const WgWork &w, const float 
     if (!direct) reduce_chunks(a, w);
 }
 
-// One direct-to-LDS 16-byte load per lane: lane l's 16 bytes from src land
-// at lds_dst + 16 l (lds_dst uniform across the wave).  Issued as inline
-// assembly so that the compiler does not track it: its wait-count pass
-// handles direct-to-LDS writes coarsely and would drain every outstanding
-// load before each later LDS read.  The caller waits for it explicitly
-// (s_waitcnt vmcnt) before the barrier that publishes the data; loads the
-// compiler does track and issues later are younger, so its own waits stay
-// sufficient.
-__device__ inline void load_lds_x16(const void *src, const uint4 *lds_dst) {
-    const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds_dst);
-    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" :: "s"(m0), "v"(src) : "memory", "m0");
-}
-
-// Barrier for LDS hand-off only.  __syncthreads() also waits for every
-// outstanding global load, which would drain the weight prefetch.
-__device__ inline void lds_barrier() {
-    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
-
 // ---- SKINNY: matrix-core dequantization + v_mfma_f32_16x16x32_bf16 --------
 //
 // A workgroup owns K chunk c (groups [g0, g0 + Kc)) of column tiles

@@ -33,13 +33,12 @@ struct qlin_s {
     int counters_n = 0;
 };
 
+namespace qlin {
+
 namespace {
-
-constexpr int kWsRowsMin = 128;        // S * M always allowed by the partial-sum workspace
-constexpr int64_t kMaxK = 65536, kMaxN = 1 << 20, kMaxM = 65536;
-
 thread_local char g_err[512] = "";
 thread_local int g_status = QLIN_OK;
+}  // namespace
 
 int fail(int code, const char *fmt, ...) {
     g_status = code;
@@ -58,6 +57,15 @@ void clear_err() {
 int hip_fail(hipError_t e, const char *what) {
     return fail(QLIN_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
+
+int last_status() { return g_status; }
+
+}  // namespace qlin
+
+namespace {
+
+constexpr int kWsRowsMin = 128;        // S * M always allowed by the partial-sum workspace
+constexpr int64_t kMaxK = 65536, kMaxN = 1 << 20, kMaxM = 65536;
 
 // Test hook: QLIN_FAULT=alloc makes every device allocation of this library fail.
 hipError_t dev_alloc(void **p, size_t bytes) {

@@ -26,7 +26,8 @@ PATH_AUTO, PATH_GEMV, PATH_SKINNY, PATH_TILED, PATH_REGS = 0, 1, 2, 3, 4
 # every symbol include/qlin.h declares
 EXPORTS = ("qlin_create", "qlin_create_symmetric", "qlin_forward", "qlin_forward_path",
            "qlin_plan", "qlin_destroy", "qlin_last_error", "qlin_unpack_codes",
-           "qlin_dequantize", "qlin_shape", "qlin_last_status", "qlin_stream_read", "qlin_quantize")
+           "qlin_dequantize", "qlin_shape", "qlin_last_status", "qlin_stream_read", "qlin_quantize",
+           "qlin_swa_plan", "qlin_swa_attention")
 
 _lib = None
 
@@ -70,6 +71,11 @@ def lib():
     L.qlin_dequantize.argtypes = [P, I32, VP, VP]
     L.qlin_stream_read.restype = I32
     L.qlin_stream_read.argtypes = [VP, I64, I32, VP, VP]
+    L.qlin_swa_plan.restype = I32
+    L.qlin_swa_plan.argtypes = [I64, I64, I64, I64, I64, I64, I64, ctypes.POINTER(I64), ctypes.POINTER(I64),
+                                ctypes.c_char_p, I64]
+    L.qlin_swa_attention.restype = I32
+    L.qlin_swa_attention.argtypes = [I64, I64, I64, I64, I64, I64, I64, I64, VP, VP, VP, VP, VP, I64, VP]
     L.qlin_shape.restype = I32
     L.qlin_shape.argtypes = [P, ctypes.POINTER(I64), ctypes.POINTER(I64)]
     _lib = L
@@ -181,7 +187,51 @@ def qlin_shape(h):
     return K.value, N.value
 
 
-# ---------------------------------------------------------------- torch wrapper
+def qlin_swa_plan(Hq, Hkv, head_dim, nq, T, window, splits=0):
+    """(splits, workspace_bytes, text) of the drafter attention's plan."""
+    S, ws = ctypes.c_int64(), ctypes.c_int64()
+    buf = ctypes.create_string_buffer(256)
+    _check(lib().qlin_swa_plan(Hq, Hkv, head_dim, nq, T, window, splits, ctypes.byref(S), ctypes.byref(ws),
+                               buf, len(buf)))
+    return S.value, ws.value, buf.value.decode()
+
+
+def qlin_swa_attention(Hq, Hkv, head_dim, nq, T, kv_stride, window, splits, q_ptr, k_ptr, v_ptr, out_ptr,
+                       ws_ptr, ws_bytes, stream):
+    return lib().qlin_swa_attention(Hq, Hkv, head_dim, nq, T, kv_stride, window, splits, q_ptr, k_ptr, v_ptr,
+                                    out_ptr, ws_ptr, ws_bytes, stream)
+
+
+# ---------------------------------------------------------------- torch wrappers
+
+def swa_attention(q, k, v, window, T=None, splits=0, out=None, workspace=None):
+    """Drafter block attention with a symmetric window (include/qlin_attn.h).
+
+    q: CUDA bf16 [Hq, nq, 128]; k, v: CUDA bf16 [Hkv, capacity, 128] with the
+    first T tokens valid (T defaults to the capacity); window 0 = full
+    attention.  ``workspace`` (a CUDA tensor of at least the planned bytes) is
+    allocated when needed and not given.  Returns ``out`` [Hq, nq, 128].
+    """
+    import torch
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if t.dtype != torch.bfloat16 or not t.is_cuda or t.dim() != 3 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous CUDA bf16 tensor of rank 3")
+    Hq, nq, D = q.shape
+    Hkv, cap, _ = k.shape
+    if v.shape != k.shape:
+        raise ValueError("k and v must have the same shape")
+    T = cap if T is None else T
+    S, ws_bytes, _ = qlin_swa_plan(Hq, Hkv, D, nq, T, window, splits)
+    if out is None:
+        out = torch.empty((Hq, nq, D), dtype=torch.bfloat16, device=q.device)
+    if ws_bytes and workspace is None:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
+    ws_ptr = workspace.data_ptr() if workspace is not None else None
+    ws_len = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(qlin_swa_attention(Hq, Hkv, D, nq, T, cap, window, splits, q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                              out.data_ptr(), ws_ptr, ws_len, torch.cuda.current_stream().cuda_stream))
+    return out
+
 
 class QLinear:
     """One W4A16 linear layer on the current GPU.

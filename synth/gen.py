@@ -125,3 +125,42 @@ def random_case(seed, M, K, N, s_range=(0.002, 0.02), z_values=(7, 8, 9),
     packed, scales, zeros = draw_weights(rng, K, N, s_range, z_values)
     x = draw_activations(rng, M, K, sigma, outlier_p)
     return dict(M=M, K=K, N=N, packed=packed, scales=scales, zeros=zeros, x=x)
+
+
+# ---------------------------------------------------------------- drafter attention
+#
+# Block attention of the drafter: 32 query heads over 8 key/value heads of
+# dimension 128 (the q/k/v projection widths 4096/1024/1024 of the layer
+# shapes above), 16 block queries, a key/value cache of T tokens.  Keys and
+# values are N(0, 1); queries are N(0, sigma_q^2), so that the scaled scores
+# q.k / sqrt(128) have standard deviation sigma_q (a moderately peaked
+# softmax).  All drawn in binary32 and rounded to bf16; draw order q, k, v.
+ATTN_HQ, ATTN_HKV, ATTN_D, ATTN_NQ = 32, 8, 128, 16
+
+ATTN_CONFIGS = {
+    # long-input decode with the leaderboard window, its wider variant and
+    # full attention (the window sweep's end points)
+    "swa1024": dict(T=8192, window=1024, sigma_q=2.0, seed=11),
+    "swa2048": dict(T=8192, window=2048, sigma_q=2.0, seed=11),
+    "full": dict(T=8192, window=0, sigma_q=2.0, seed=11),
+    # a short prompt inside the window (full-attention fallback)
+    "short": dict(T=700, window=1024, sigma_q=2.0, seed=12),
+}
+
+
+def draw_attention(rng, Hq, Hkv, nq, T, sigma_q=2.0, D=ATTN_D, kv_stride=None):
+    """q [Hq][nq][D], k and v [Hkv][kv_stride][D] as bf16 bits (tokens at and
+    beyond T up to kv_stride are drawn too: they stand for unused capacity)."""
+    kv_stride = T if kv_stride is None else kv_stride
+    q = rng.standard_normal((Hq, nq, D), dtype=np.float32) * np.float32(sigma_q)
+    k = rng.standard_normal((Hkv, kv_stride, D), dtype=np.float32)
+    v = rng.standard_normal((Hkv, kv_stride, D), dtype=np.float32)
+    return f32_to_bf16_bits(q), f32_to_bf16_bits(k), f32_to_bf16_bits(v)
+
+
+def attention_case(name):
+    """One drafter attention workload: dict(Hq, Hkv, nq, T, window, q, k, v)."""
+    c = ATTN_CONFIGS[name]
+    rng = np.random.default_rng(c["seed"])
+    q, k, v = draw_attention(rng, ATTN_HQ, ATTN_HKV, ATTN_NQ, c["T"], c["sigma_q"])
+    return dict(Hq=ATTN_HQ, Hkv=ATTN_HKV, nq=ATTN_NQ, T=c["T"], window=c["window"], q=q, k=k, v=v)

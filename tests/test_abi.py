@@ -1,4 +1,4 @@
-"""The C ABI library loads, exports what include/qlin.h declares, and rejects
+"""The C ABI library loads, exports what include/*.h declare, and rejects
 bad arguments before any HIP call (CPU only: no compute is launched)."""
 
 import os
@@ -14,9 +14,13 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def _declared_functions():
-    txt = open(os.path.join(ROOT, "include", "qlin.h")).read()
-    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
-    return sorted(set(re.findall(r"\b(qlin_[a-z_]+)\s*\(", txt)))
+    names = set()
+    inc = os.path.join(ROOT, "include")
+    for f in sorted(os.listdir(inc)):
+        if f.endswith(".h"):
+            txt = re.sub(r"/\*.*?\*/", "", open(os.path.join(inc, f)).read(), flags=re.S)
+            names |= set(re.findall(r"\b(qlin_[a-z_]+)\s*\(", txt))
+    return sorted(names)
 
 
 def test_header_declares_the_binding_names():
@@ -153,3 +157,71 @@ def test_quantize_rejects_bad_arguments():
     assert f(256, 32, 128, A, A + 1, A, 2 * A, None) == qlin.QLIN_ERR_ALIGN
     assert f(256, 32, 128, A, A, A, A + 256, None) == qlin.QLIN_ERR_INVALID      # packed overlaps w
     assert "overlaps" in qlin.last_error()
+
+
+# ---------------------------------------------------------------- drafter attention
+
+def test_attention_plan_key_ranges():
+    """Explicit splits need no device: the plan is pure arithmetic."""
+    # window 1024 at T = 8192: keys [8192 - 16 - 512, 8192) = 528 keys, 9 tiles of 64
+    S, ws, txt = qlin.qlin_swa_plan(32, 8, 128, 16, 8192, 1024, 3)
+    assert S == 3 and ws == 3 * 32 * 16 * 130 * 4 and "keys=528 tiles=9" in txt and "grid=24" in txt
+    # T <= window: full attention over all T keys
+    S, ws, txt = qlin.qlin_swa_plan(32, 8, 128, 16, 700, 1024, 100)
+    assert S == 11 and "keys=700 tiles=11" in txt
+    # window 0: full attention; one split needs no workspace
+    S, ws, txt = qlin.qlin_swa_plan(4, 1, 128, 1, 5, 0, 1)
+    assert (S, ws) == (1, 0) and "combine=0" in txt
+    # splits that do not divide the tiles: no empty range
+    S, _, _ = qlin.qlin_swa_plan(8, 8, 128, 16, 64 * 10, 0, 4)
+    assert S == 4          # 3 tiles per range: 3 + 3 + 3 + 1
+    S, _, _ = qlin.qlin_swa_plan(8, 8, 128, 16, 64 * 10, 0, 6)
+    assert S == 5          # 2 tiles per range
+    _, _, txt = qlin.qlin_swa_plan(64, 8, 128, 16, 100, 0, 1)
+    assert "k_attn_split<2>" in txt
+
+
+@pytest.mark.parametrize("args,code", [
+    ((32, 8, 64, 16, 100, 0, 1), qlin.QLIN_ERR_UNSUPPORTED),     # head_dim
+    ((128, 8, 128, 16, 100, 0, 1), qlin.QLIN_ERR_UNSUPPORTED),   # 16 query heads per key/value head
+    ((30, 8, 128, 16, 100, 0, 1), qlin.QLIN_ERR_INVALID),        # Hq not a multiple of Hkv
+    ((0, 8, 128, 16, 100, 0, 1), qlin.QLIN_ERR_INVALID),
+    ((32, 8, 128, 0, 100, 0, 1), qlin.QLIN_ERR_INVALID),         # nq
+    ((32, 8, 128, 17, 100, 0, 1), qlin.QLIN_ERR_INVALID),
+    ((32, 8, 128, 16, 15, 0, 1), qlin.QLIN_ERR_INVALID),         # T < nq
+    ((32, 8, 128, 16, 2 ** 28 + 1, 0, 1), qlin.QLIN_ERR_INVALID),
+    ((32, 8, 128, 16, 100, -1, 1), qlin.QLIN_ERR_INVALID),       # window
+    ((32, 8, 128, 16, 100, 0, -1), qlin.QLIN_ERR_INVALID),       # splits
+])
+def test_attention_plan_rejects_bad_sizes(args, code):
+    with pytest.raises(qlin.QlinError) as e:
+        qlin.qlin_swa_plan(*args)
+    assert e.value.code == code
+
+
+def test_attention_rejects_bad_arguments():
+    """Every case fails in the argument checks, before any HIP call."""
+    A = 1 << 32                    # fake, 16-byte aligned addresses (never dereferenced)
+    q, k, v, o, w = A, A + (1 << 24), A + (2 << 24), A + (3 << 24), A + (4 << 24)
+    base = dict(Hq=32, Hkv=8, D=128, nq=16, T=1000, kv_stride=1000, window=0, splits=4,
+                q=q, k=k, v=v, o=o, w=w, wb=1 << 24)
+
+    def call(**kw):
+        a = dict(base, **kw)
+        return qlin.qlin_swa_attention(a["Hq"], a["Hkv"], a["D"], a["nq"], a["T"], a["kv_stride"], a["window"],
+                                       a["splits"], a["q"], a["k"], a["v"], a["o"], a["w"], a["wb"], None)
+
+    assert call(kv_stride=999) == qlin.QLIN_ERR_INVALID
+    assert call(q=None) == qlin.QLIN_ERR_INVALID
+    assert call(o=None) == qlin.QLIN_ERR_INVALID
+    assert call(k=k + 8) == qlin.QLIN_ERR_ALIGN
+    assert call(w=w + 4) == qlin.QLIN_ERR_ALIGN
+    assert call(wb=-1) == qlin.QLIN_ERR_INVALID
+    assert call(w=None, wb=0) == qlin.QLIN_ERR_INVALID               # 4 ranges need a workspace
+    assert call(wb=4 * 32 * 16 * 130 * 4 - 16) == qlin.QLIN_ERR_INVALID
+    assert "workspace" in qlin.last_error()
+    assert call(o=q + 1024) == qlin.QLIN_ERR_INVALID                 # out overlaps q
+    assert call(o=v + 7 * 1000 * 256) == qlin.QLIN_ERR_INVALID       # out overlaps the last head of v
+    assert call(o=w + 4096) == qlin.QLIN_ERR_INVALID                 # out overlaps the workspace
+    assert call(D=96) == qlin.QLIN_ERR_UNSUPPORTED
+    assert qlin.qlin_last_status() == qlin.QLIN_ERR_UNSUPPORTED
