@@ -57,7 +57,7 @@ extern "C" {
  * Outputs (each may be NULL): *splits_out = the key ranges per key/value
  * head; *workspace_bytes = the device workspace qlin_swa_attention needs
  * (0 when one range suffices); buf = NUL-terminated text such as
- * "kernel=k_attn_split<1> keys=528 tiles=9 splits=9 grid=72 combine=1"
+ * "kernel=k_attn_split<1,4> keys=528 tiles=9 splits=9 grid=72 combine=1"
  * (at most buflen bytes; buf may be NULL).
  * Errors: INVALID (sizes out of range), UNSUPPORTED (head_dim != 128,
  * Hq / Hkv > 8), HIP (device query).

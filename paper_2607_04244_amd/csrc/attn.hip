@@ -15,9 +15,9 @@
 //       v_mfma_f32_16x16x32_bf16 with an online softmax in fp32.  With one
 //       split the workgroup writes the bf16 output; otherwise it writes its
 //       unnormalised partial output and (max, sum) per query row.
-//   k_attn_combine     one workgroup per (query head, query row): rescales
-//       the partials of every split and sums them in a fixed order
-//       (deterministic).
+//   k_attn_combine     one workgroup per (query head, 16 dimensions):
+//       folds the partials of every split in with a running maximum, in a
+//       fixed order (deterministic).
 //
 // MFMA operand layouts (16x16x32 bf16, lane l, g = l >> 4, r = l & 15):
 //   A: row r, k = 8 g + e;  B: column r, k = 8 g + e;  D: column r, rows 4 g + i.
@@ -35,7 +35,6 @@ namespace {
 constexpr int kTileUnits = kAttnTile * kAttnD / 8;   // 16-byte units of one K or V tile (1024)
 constexpr int kQUnits = kAttnQ * kAttnD / 8;         // 16-byte units of one head's block queries (256)
 constexpr int kSplitWaves = 2 * kAttnWaves;          // two waves per query head: one per 32-key half
-constexpr int kStages = 3;                           // tiles in flight per workgroup
 constexpr int kTileLoads = 4;                        // direct-to-LDS loads per wave and tile (2 K + 2 V)
 constexpr float kNegInf = -__builtin_huge_valf();
 
@@ -58,18 +57,19 @@ __device__ inline v4s_t lds_read_tr(const void *p) {
 __device__ inline int tile_unit(int kk, int c) { return kk * 16 + (c ^ (kk & 15)); }
 
 // Every global read of the split kernel is a direct-to-LDS load (untracked
-// by the compiler, waited for explicitly), so up to kStages tiles stream in
-// while earlier ones are computed:
+// by the compiler, waited for explicitly).  The ring holds NS tiles: all NS
+// are requested at the start, and each later tile as soon as its slot has
+// been consumed, so NS - 1 tiles stream in while one is computed:
 //   qs     the block queries of this workgroup's heads, 16 rows x 16 units,
 //          unit c of row r at r * 16 + (c ^ r)
 //   kring  K tiles, vring V tiles, both in the tile_unit layout
 // Wave w takes query head w % 4 (and w % 4 + 4 when G > 4) and keys
 // 32 (w / 4) .. + 31 of every tile; the two halves of a head are merged
 // through LDS at the end.
-template <int HPW>
+template <int HPW, int NS>
 __global__ __launch_bounds__(kSplitWaves * 64, 1) void k_attn_split(AttnArgs a) {
     __shared__ __attribute__((aligned(16))) uint4 qs[HPW * kAttnWaves * kQUnits];
-    __shared__ __attribute__((aligned(16))) uint4 ring[2][kStages][kTileUnits];   // K tiles, V tiles
+    __shared__ __attribute__((aligned(16))) uint4 ring[2][NS][kTileUnits];   // K tiles, V tiles
     uint4 (*kring)[kTileUnits] = ring[0];
     uint4 (*vring)[kTileUnits] = ring[1];
 
@@ -105,7 +105,7 @@ __global__ __launch_bounds__(kSplitWaves * 64, 1) void k_attn_split(AttnArgs a) 
     }
 
     auto issue = [&](int t) {
-        const int st = t % kStages;
+        const int st = t % NS;
         const int key0 = a.lo + t * kAttnTile;
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
@@ -115,7 +115,7 @@ __global__ __launch_bounds__(kSplitWaves * 64, 1) void k_attn_split(AttnArgs a) 
             load_lds_x16(vh + (size_t)key * kAttnD + 8 * c, &vring[st][(kSplitWaves * j + wave) * 64]);
         }
     };
-    for (int t = t0; t < min(t0 + kStages - 1, t1); ++t) issue(t);
+    for (int t = t0; t < min(t0 + NS, t1); ++t) issue(t);
 
     float m[HPW], l[HPW];
     v4f o[HPW][8];
@@ -142,12 +142,15 @@ __global__ __launch_bounds__(kSplitWaves * 64, 1) void k_attn_split(AttnArgs a) 
     const int tj = r >> 2, tq = r & 3;
 
     for (int t = t0; t < t1; ++t) {
-        const int st = t % kStages;
-        // this wave's loads of tile t (and the queries) are complete
-        if (t + 1 < t1) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(kTileLoads) : "memory");
+        const int st = t % NS;
+        // this wave's loads of tile t (and the queries) are complete: the
+        // tiles requested after t may still be in flight
+        const int after = min(t1 - 1, t + NS - 1) - t;
+        if (after >= 3) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(3 * kTileLoads) : "memory");
+        else if (after == 2) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * kTileLoads) : "memory");
+        else if (after == 1) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(kTileLoads) : "memory");
         else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-        lds_barrier();                 // tile t visible to all waves; every wave is done with tile t - 1
-        if (t + kStages - 1 < t1) issue(t + kStages - 1);
+        lds_barrier();                 // tile t visible to all waves
         if (t == t0) {
 #pragma unroll
             for (int hh = 0; hh < HPW; ++hh)
@@ -224,6 +227,10 @@ __global__ __launch_bounds__(kSplitWaves * 64, 1) void k_attn_split(AttnArgs a) 
                 o[hh][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pb, o[hh][dt], 0, 0, 0);
             }
         }
+        if (t + NS < t1) {
+            lds_barrier();             // every wave is done with slot st
+            issue(t + NS);
+        }
     }
 
     // merge the two key halves of each head: the second wave hands (m, l, o)
@@ -232,6 +239,7 @@ __global__ __launch_bounds__(kSplitWaves * 64, 1) void k_attn_split(AttnArgs a) 
     float *xs = (float *)&ring[0][0][0];
     constexpr int kXch = 64 * (2 + 32);                     // floats per (wave, head)
     static_assert(HPW * kAttnWaves * kXch * 4 <= (int)sizeof(ring), "exchange fits the rings");
+    static_assert(NS <= 4, "wait counts cover at most three tiles in flight behind the current one");
     __syncthreads();
 #pragma unroll
     for (int hh = 0; hh < HPW; ++hh) {
@@ -279,100 +287,88 @@ __global__ __launch_bounds__(kSplitWaves * 64, 1) void k_attn_split(AttnArgs a) 
                 *(uint2 *)(op + 16 * dt) = w;
             }
         } else {
-            float *wp = a.ws_o + (row * a.S + s) * kAttnD + 4 * g;
+            // partials of (head, split): 8 blocks (one per 16 dimensions) of
+            // 16 rows x 16 fp32, so each store instruction fills 1 KiB
+            const size_t hs = (size_t)hq[hh] * a.S + s;
+            float *wp = a.ws_o + hs * 8 * 256 + r * 16 + 4 * g;
 #pragma unroll
-            for (int dt = 0; dt < 8; ++dt) *(v4f *)(wp + 16 * dt) = o[hh][dt];
-            if (g == 0) *(float2 *)(a.ws_ml + (row * a.S + s) * 2) = make_float2(m[hh], lt);
+            for (int dt = 0; dt < 8; ++dt) *(v4f *)(wp + dt * 256) = o[hh][dt];
+            if (g == 0) *(float2 *)(a.ws_ml + (hs * 16 + r) * 2) = make_float2(m[hh], lt);
         }
     }
 }
 
-// One workgroup of 128 threads per (query head, query row).  Thread t sums
-// splits s = t / 32 (mod 4) for dimensions 4 (t % 32) .. + 3, each split's
-// partial scaled by exp2((m_s - M) c); the four partial sums are added in
-// a fixed order, so the result does not depend on timing.
-constexpr int kCombThreads = 128;
-constexpr int kCombPrefetch = 8;   // partial rows loaded ahead per thread
+// One workgroup of 4 waves per (query head, 16 dimensions).  Thread
+// (g, r) of wave sg owns query row r, dimensions 16 dt + 4 g .. + 3, and
+// splits s = sg, sg + 4, ...: it requests all of them at once, folds them in
+// with a running maximum, and the four waves' results are merged in wave
+// order through LDS, so the result does not depend on timing.
+constexpr int kCombWaves = 4;
+constexpr int kCombBatch = 8;      // splits per thread requested together
 
-__global__ __launch_bounds__(kCombThreads) void k_attn_combine(AttnArgs a) {
-    __shared__ float es[kAttnMaxSplits];
-    __shared__ float red[2][2];
-    __shared__ __attribute__((aligned(16))) float4 part[4][32];
-    const size_t row = blockIdx.x;
-    const int t = threadIdx.x, lane = t & 63, wv = t >> 6;
-    const int dq = t & 31, sp = t >> 5;
-    const float2 *ml = (const float2 *)(a.ws_ml + row * a.S * 2);
-    const float4 *po = (const float4 *)(a.ws_o + row * a.S * kAttnD) + dq;
+struct CombState { float m, l; float4 acc; };
 
-    // partial outputs of the first splits, loaded before the weights are known
-    float4 pre[kCombPrefetch];
-#pragma unroll
-    for (int i = 0; i < kCombPrefetch; ++i) {
-        const int sidx = sp + 4 * i;
-        pre[i] = sidx < a.S ? po[(size_t)sidx * (kAttnD / 4)] : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-    float mx = kNegInf;
-    for (int si = t; si < a.S; si += kCombThreads) mx = fmaxf(mx, ml[si].x);
-#pragma unroll
-    for (int k = 32; k >= 1; k >>= 1) mx = fmaxf(mx, shfl_xor_f(mx, k));
-    if (lane == 0) red[0][wv] = mx;
-    __syncthreads();
-    const float M = fmaxf(red[0][0], red[0][1]);
+__device__ inline void comb_fold(CombState &st, float m2, float l2, const float4 &v, float c) {
+    const float M = fmaxf(st.m, m2);
     const float mu = M == kNegInf ? 0.0f : M;
-    float ls = 0.0f;
-    for (int si = t; si < a.S; si += kCombThreads) {
-        const float2 e = ml[si];
-        const float f = __builtin_amdgcn_exp2f((e.x - mu) * a.c);
-        es[si] = f;
-        ls += f * e.y;
-    }
-#pragma unroll
-    for (int k = 32; k >= 1; k >>= 1) ls += shfl_xor_f(ls, k);
-    if (lane == 0) red[1][wv] = ls;
-    __syncthreads();
-    const float L = red[1][0] + red[1][1];
+    const float f1 = __builtin_amdgcn_exp2f((st.m - mu) * c), f2 = __builtin_amdgcn_exp2f((m2 - mu) * c);
+    st.m = M;
+    st.l = st.l * f1 + l2 * f2;
+    st.acc.x = st.acc.x * f1 + v.x * f2;
+    st.acc.y = st.acc.y * f1 + v.y * f2;
+    st.acc.z = st.acc.z * f1 + v.z * f2;
+    st.acc.w = st.acc.w * f1 + v.w * f2;
+}
 
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+__global__ __launch_bounds__(kCombWaves * 64) void k_attn_combine(AttnArgs a) {
+    __shared__ CombState xs[kCombWaves][64];
+    const int hq = blockIdx.x >> 3, dt = blockIdx.x & 7;
+    const int lane = threadIdx.x & 63, sg = threadIdx.x >> 6;
+    const int r = lane & 15, g = lane >> 4;
+    const float2 *ml = (const float2 *)a.ws_ml + (size_t)hq * a.S * 16 + r;          // + 16 s
+    const float4 *po = (const float4 *)(a.ws_o + ((size_t)hq * a.S * 8 + dt) * 256 + r * 16 + 4 * g);   // + 512 s
+    CombState st{kNegInf, 0.0f, make_float4(0.f, 0.f, 0.f, 0.f)};
+    if (r < a.nq) {
+        for (int s0 = sg; s0 < a.S; s0 += kCombWaves * kCombBatch) {
+            float2 e[kCombBatch];
+            float4 v[kCombBatch];
 #pragma unroll
-    for (int i = 0; i < kCombPrefetch; ++i) {
-        const int sidx = sp + 4 * i;
-        const float f = sidx < a.S ? es[sidx] : 0.0f;
-        acc.x += f * pre[i].x;
-        acc.y += f * pre[i].y;
-        acc.z += f * pre[i].z;
-        acc.w += f * pre[i].w;
+            for (int i = 0; i < kCombBatch; ++i) {
+                const int si = s0 + kCombWaves * i;
+                e[i] = si < a.S ? ml[(size_t)si * 16] : make_float2(kNegInf, 0.0f);
+                v[i] = si < a.S ? po[(size_t)si * 512] : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int i = 0; i < kCombBatch; ++i) comb_fold(st, e[i].x, e[i].y, v[i], a.c);
+        }
     }
-    for (int sidx = sp + 4 * kCombPrefetch; sidx < a.S; sidx += 4) {
-        const float f = es[sidx];
-        const float4 v = po[(size_t)sidx * (kAttnD / 4)];
-        acc.x += f * v.x;
-        acc.y += f * v.y;
-        acc.z += f * v.z;
-        acc.w += f * v.w;
-    }
-    part[sp][dq] = acc;
+    xs[sg][lane] = st;
     __syncthreads();
-    if (t < 32) {
-        const float4 p0 = part[0][t], p1 = part[1][t], p2 = part[2][t], p3 = part[3][t];
-        uint2 w;
-        w.x = cvt_pk_bf16((((p0.x + p1.x) + p2.x) + p3.x) / L, (((p0.y + p1.y) + p2.y) + p3.y) / L);
-        w.y = cvt_pk_bf16((((p0.z + p1.z) + p2.z) + p3.z) / L, (((p0.w + p1.w) + p2.w) + p3.w) / L);
-        *(uint2 *)(a.out + row * kAttnD + 4 * t) = w;
+    if (sg != 0 || r >= a.nq) return;
+#pragma unroll
+    for (int w = 1; w < kCombWaves; ++w) {
+        const CombState o = xs[w][lane];
+        comb_fold(st, o.m, o.l, o.acc, a.c);
     }
+    uint2 w;
+    w.x = cvt_pk_bf16(st.acc.x / st.l, st.acc.y / st.l);
+    w.y = cvt_pk_bf16(st.acc.z / st.l, st.acc.w / st.l);
+    *(uint2 *)(a.out + ((size_t)hq * a.nq + r) * kAttnD + 16 * dt + 4 * g) = w;
 }
 
 }  // namespace
 
-const char *attn_kernel_name(int G) { return G > kAttnWaves ? "k_attn_split<2>" : "k_attn_split<1>"; }
+const char *attn_kernel_name(int G) { return G > kAttnWaves ? "k_attn_split<2,3>" : "k_attn_split<1,4>"; }
 
 hipError_t launch_attn(const AttnArgs &a, hipStream_t st) {
     const dim3 block(kSplitWaves * 64);
     const dim3 grid((unsigned)(a.Hkv * a.S));
-    if (a.G > kAttnWaves) hipLaunchKernelGGL(k_attn_split<2>, grid, block, 0, st, a);
-    else hipLaunchKernelGGL(k_attn_split<1>, grid, block, 0, st, a);
+    // one head per wave: four tiles in flight (144 KiB of LDS); two heads: three (128 KiB)
+    if (a.G > kAttnWaves) hipLaunchKernelGGL((k_attn_split<2, 3>), grid, block, 0, st, a);
+    else hipLaunchKernelGGL((k_attn_split<1, 4>), grid, block, 0, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.S == 1) return e;
-    hipLaunchKernelGGL(k_attn_combine, dim3((unsigned)(a.Hq * a.nq)), dim3(kCombThreads), 0, st, a);
+    hipLaunchKernelGGL(k_attn_combine, dim3((unsigned)(a.Hq * 8)), dim3(kCombWaves * 64), 0, st, a);
     return hipGetLastError();
 }
 

@@ -54,7 +54,8 @@ int make_attn_plan(int64_t Hq, int64_t Hkv, int64_t nq, int64_t T, int64_t windo
     S = std::min<int64_t>({S, (int64_t)p->ntiles, (int64_t)kAttnMaxSplits});
     p->tps = (int)((p->ntiles + S - 1) / S);
     p->S = (p->ntiles + p->tps - 1) / p->tps;
-    p->ws_bytes = p->S > 1 ? (int64_t)p->S * Hq * nq * (kAttnD + 2) * 4 : 0;
+    // partials of every (head, split) cover all 16 rows of the query tile
+    p->ws_bytes = p->S > 1 ? (int64_t)p->S * Hq * kAttnQ * (kAttnD + 2) * 4 : 0;
     return QLIN_OK;
 }
 
@@ -108,7 +109,7 @@ int qlin_swa_attention(int64_t Hq, int64_t Hkv, int64_t head_dim, int64_t nq, in
     a.v = v;
     a.out = out;
     a.ws_o = (float *)workspace;
-    a.ws_ml = p.S > 1 ? (float *)workspace + (size_t)p.S * Hq * nq * kAttnD : nullptr;
+    a.ws_ml = p.S > 1 ? (float *)workspace + (size_t)p.S * Hq * kAttnQ * kAttnD : nullptr;
     a.kv_stride = kv_stride * kAttnD;
     a.Hq = (int)Hq;
     a.Hkv = (int)Hkv;

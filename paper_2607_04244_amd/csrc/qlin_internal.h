@@ -133,8 +133,8 @@ struct AttnArgs {
     const uint16_t *q;      // [Hq][nq][128] bf16
     const uint16_t *k, *v;  // [Hkv][kv_stride][128] bf16
     uint16_t *out;          // [Hq][nq][128] bf16
-    float *ws_o;            // S > 1: unnormalised partial outputs [Hq][nq][S][128]
-    float *ws_ml;           // S > 1: (running max, sum of weights) [Hq][nq][S][2]
+    float *ws_o;            // S > 1: unnormalised partial outputs [Hq][S][8][16 rows][16]
+    float *ws_ml;           // S > 1: (running max, sum of weights) [Hq][S][16 rows][2]
     int64_t kv_stride;      // elements between consecutive key/value heads
     int Hq, Hkv, G, nq, T;
     int lo, hi;             // keys [lo, hi) some block query can see

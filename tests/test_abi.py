@@ -166,6 +166,9 @@ def test_attention_plan_key_ranges():
     # window 1024 at T = 8192: keys [8192 - 16 - 512, 8192) = 528 keys, 9 tiles of 64
     S, ws, txt = qlin.qlin_swa_plan(32, 8, 128, 16, 8192, 1024, 3)
     assert S == 3 and ws == 3 * 32 * 16 * 130 * 4 and "keys=528 tiles=9" in txt and "grid=24" in txt
+    # the workspace covers 16 rows per (head, split) whatever nq is
+    S, ws, _ = qlin.qlin_swa_plan(32, 8, 128, 5, 8192, 1024, 3)
+    assert S == 3 and ws == 3 * 32 * 16 * 130 * 4
     # T <= window: full attention over all T keys
     S, ws, txt = qlin.qlin_swa_plan(32, 8, 128, 16, 700, 1024, 100)
     assert S == 11 and "keys=700 tiles=11" in txt
@@ -178,7 +181,7 @@ def test_attention_plan_key_ranges():
     S, _, _ = qlin.qlin_swa_plan(8, 8, 128, 16, 64 * 10, 0, 6)
     assert S == 5          # 2 tiles per range
     _, _, txt = qlin.qlin_swa_plan(64, 8, 128, 16, 100, 0, 1)
-    assert "k_attn_split<2>" in txt
+    assert "k_attn_split<2,3>" in txt
 
 
 @pytest.mark.parametrize("args,code", [
