@@ -52,31 +52,46 @@ def algorithmic_bytes(M, K, N, symmetric=False):
     return K * N // 2 + per_group * (K // 128) * N + 2 * M * K + 2 * M * N
 
 
-def device_sources_hash():
-    """sha256 (16 hex digits) of every device source of the library, in name
-    order: identifies the kernels a stored counter summary was taken on."""
+# device sources each kernel family is built from (the stored counter
+# summary of a kernel is valid while these files are unchanged)
+KERNEL_SOURCES = {
+    "linear": ("kernels.hip", "device_common.h", "qlin_internal.h"),
+    "tiled": ("tiled.hip", "device_common.h", "qlin_internal.h"),
+    "attention": ("attn.hip", "attn_internal.h", "device_common.h", "qlin_internal.h"),
+}
+
+
+def kernel_family(kernel):
+    if kernel.startswith("k_attn"):
+        return "attention"
+    return "tiled" if kernel.startswith("k_tiled") else "linear"
+
+
+def device_sources_hash(family="linear"):
+    """sha256 (16 hex digits) of the device sources of one kernel family, in
+    name order: identifies the kernels a stored counter summary was taken on."""
     import hashlib
     d = os.path.join(ROOT, "paper_2607_04244_amd", "csrc")
     h = hashlib.sha256()
-    for name in sorted(os.listdir(d)):
-        if name.endswith((".hip", ".h")):
-            with open(os.path.join(d, name), "rb") as f:
-                h.update(name.encode() + b"\0" + f.read())
+    for name in sorted(KERNEL_SOURCES[family]):
+        with open(os.path.join(d, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()[:16]
 
 
-def traffic_from_profiles(kernel_src_hash, kernel):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, if it
-    was taken on the current kernel source; else None."""
+def traffic_from_profiles(kernel, key=None):
+    """HBM bytes per launch from the committed rocprofv3 counter summary (entry
+    `key`, default the kernel's name), if it was taken on the current source
+    of the kernel's family; else None."""
     p = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         t = json.load(open(p))
     except (OSError, ValueError):
         return None
-    if t.get("device_sources_sha256_16") != kernel_src_hash:
+    e = t.get("kernels", {}).get(key or kernel)
+    if e is None or e.get("sources_sha256_16") != device_sources_hash(kernel_family(kernel)):
         return None
-    e = t.get("kernels", {}).get(kernel)
-    return None if e is None else e.get("hbm_bytes_per_launch")
+    return e.get("hbm_bytes_per_launch")
 
 
 def cpu_baseline(case, budget_s=12.0):
@@ -273,10 +288,16 @@ def bench_attention(args, name):
     stream.synchronize()
     us, _ = graph_time_us(torch, stream, calls, reps=max(2, args.steps // R))
     gbs = nbytes / (us * 1e-6) / 1e9
+    kernel = plan.split("kernel=")[1].split()[0]
     res = {"workload": f"drafter block attention {name}: Hq={Hq}, Hkv={Hkv}, d=128, nq={nq}, T={T}, "
                        f"window={W or 'full'} ({hi - lo} visible keys per head, {R} rotating caches)",
            "us_per_call": round(us, 3), "bytes_per_call": nbytes, "GBps": round(gbs, 1),
-           "pct_of_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2), "plan": plan}
+           "pct_of_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2), "plan": plan,
+           "roofline": {"bound": "hbm", "kernel": kernel + (" + k_attn_combine" if S > 1 else ""),
+                        "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(gbs / PEAK_HBM_GBS, 4),
+                        "traffic": traffic_from_profiles(kernel, f"call@{name}"),
+                        "bytes_per_launch": nbytes, "avg_launch_us": round(us, 3)}}
     if not args.no_cpu:
         times = []
         t_start = time.perf_counter()
@@ -285,8 +306,15 @@ def bench_attention(args, name):
             ar.swa_attention(c["q"], c["k"], c["v"], W)
             times.append(time.perf_counter() - t0)
         t = float(np.median(times))
-        res["cpu_baseline"] = {"value": round(nbytes / t / 1e9, 4), "unit": "GB/s", "kind": "oracle",
-                               "sample": f"{len(times)} whole oracle calls (median {t:.3f} s)"}
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        except Exception:
+            threads = 1
+        res["cpu_baseline"] = {"value": round(nbytes / t / 1e9, 4), "unit": "GB/s", "cores": int(threads),
+                               "kind": "oracle",
+                               "sample": f"{len(times)} whole oracle calls (median {t:.3f} s; float64 numpy, "
+                                         f"matmuls on {threads} BLAS threads)"}
     print(json.dumps(res), flush=True)
 
 
@@ -389,8 +417,7 @@ def main():
     ceil_gbs, ceil_us = stream_read_ceiling(torch, qlin, bytes_step, stream)
 
     kernel = plan.split("kernel=")[1].split()[0] if "kernel=" in plan else "?"
-    src_hash = device_sources_hash()
-    traffic = traffic_from_profiles(src_hash, kernel)
+    traffic = traffic_from_profiles(kernel)
     wl = {"verify": "draft-block verification linear: M=16, K=2560, N=19456 (fused gate+up)"}.get(
         args.workload, f"{args.workload}: M={M}, K={K}, N={N}")
     out = {

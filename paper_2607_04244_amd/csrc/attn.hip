@@ -26,6 +26,7 @@
 // keys when the k index e of group g stands for key 4 g + e (e < 4) or
 // 16 + 4 g + (e - 4) (e >= 4).  The transposed V rows in LDS store keys in
 // that order, so no register shuffle is needed between the two products.
+#include "attn_internal.h"
 #include "device_common.h"
 
 namespace qlin {

@@ -9,6 +9,7 @@
 #include <cmath>
 #include <cstdio>
 
+#include "attn_internal.h"
 #include "qlin_internal.h"
 
 using namespace qlin;
