@@ -42,7 +42,27 @@ constexpr float kNegInf = -__builtin_huge_valf();
 typedef short v4s_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s_t lds_v4s;
 
-__device__ inline float shfl_xor_f(float v, int m) { return __shfl_xor(v, m, 64); }
+// Cross-lane pair reductions without LDS (gfx950 v_permlane{16,32}_swap):
+// swapping a register with itself returns, in every lane, the values of the
+// lane pair {l, l ^ 16} (resp. {l, l ^ 32}) in the same order for both
+// lanes, so both lanes of a pair compute identical results.
+__device__ inline float pair16_max(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float pair32_max(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float pair16_sum(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ inline float pair32_sum(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+constexpr uint32_t kBf16OnePair = 0x3F803F80u;       // bf16 (1.0, 1.0)
 
 // Transposing LDS read (ds_read_b64_tr_b16): within each group of 16 lanes,
 // lane i receives element i & 3 of the 8-byte chunks addressed by lanes
@@ -77,7 +97,18 @@ __global__ __launch_bounds__(kSplitWaves * 64, 1) void k_attn_split(AttnArgs a) 
     const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
     const int g = lane >> 4, r = lane & 15;
     const int hw = wave & (kAttnWaves - 1), half = wave >> 2;
-    const int h = blockIdx.x / a.S, s = blockIdx.x - h * a.S;
+    // XCD-aware placement (workgroup b runs on XCD b % 8): with a multiple of
+    // 8 key/value heads, every split of head h runs on XCD h % 8, so the
+    // head's queries are fetched from HBM once and its partials stay in one L2
+    int h, s;
+    if ((a.Hkv & 7) == 0) {
+        const int q8 = blockIdx.x >> 3, hb = q8 / a.S;
+        h = (blockIdx.x & 7) + 8 * hb;
+        s = q8 - hb * a.S;
+    } else {
+        h = blockIdx.x / a.S;
+        s = blockIdx.x - h * a.S;
+    }
     const int t0 = s * a.tps, t1 = min(t0 + a.tps, a.ntiles);
     const uint16_t *kh = a.k + (size_t)h * a.kv_stride;
     const uint16_t *vh = a.v + (size_t)h * a.kv_stride;
@@ -191,12 +222,11 @@ __global__ __launch_bounds__(kSplitWaves * 64, 1) void k_attn_split(AttnArgs a) 
             }
             float mt = fmaxf(fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3])),
                              fmaxf(fmaxf(sc[1][0], sc[1][1]), fmaxf(sc[1][2], sc[1][3])));
-            mt = fmaxf(mt, shfl_xor_f(mt, 16));
-            mt = fmaxf(mt, shfl_xor_f(mt, 32));
+            mt = pair32_max(pair16_max(mt));
             const float mn = fmaxf(m[hh], mt);
-            const float mu = mn == kNegInf ? 0.0f : mn;
+            const float muc = (mn == kNegInf ? 0.0f : mn) * a.c;   // exponents are s c - m c
             if (__ballot(mn != m[hh])) {                    // some row maximum moved: rescale
-                const float alpha = __builtin_amdgcn_exp2f((m[hh] - mu) * a.c);
+                const float alpha = __builtin_amdgcn_exp2f(__builtin_fmaf(m[hh], a.c, -muc));
                 l[hh] *= alpha;
 #pragma unroll
                 for (int dt = 0; dt < 8; ++dt) o[hh][dt] *= alpha;
@@ -209,11 +239,11 @@ __global__ __launch_bounds__(kSplitWaves * 64, 1) void k_attn_split(AttnArgs a) 
             for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
                 for (int i2 = 0; i2 < 2; ++i2) {
-                    const float e0 = __builtin_amdgcn_exp2f((sc[kt][2 * i2] - mu) * a.c);
-                    const float e1 = __builtin_amdgcn_exp2f((sc[kt][2 * i2 + 1] - mu) * a.c);
+                    const float e0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[kt][2 * i2], a.c, -muc));
+                    const float e1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[kt][2 * i2 + 1], a.c, -muc));
                     const uint32_t w = cvt_pk_bf16(e0, e1);
                     pw[kt][i2] = w;
-                    ls += bf16_lo_to_f32(w) + bf16_hi_to_f32(w);
+                    ls = dot2(w, kBf16OnePair, ls);         // + both rounded weights
                 }
             l[hh] += ls;
             // O^T += V^T P^T over this wave's 32 keys
@@ -273,9 +303,7 @@ __global__ __launch_bounds__(kSplitWaves * 64, 1) void k_attn_split(AttnArgs a) 
 #pragma unroll
     for (int hh = 0; hh < HPW; ++hh) {
         if (!has[hh]) continue;
-        float lt = l[hh];
-        lt += shfl_xor_f(lt, 16);
-        lt += shfl_xor_f(lt, 32);
+        const float lt = pair32_sum(pair16_sum(l[hh]));
         if (r >= a.nq) continue;
         const size_t row = (size_t)hq[hh] * a.nq + r;
         if (a.S == 1) {
@@ -323,7 +351,17 @@ __device__ inline void comb_fold(CombState &st, float m2, float l2, const float4
 
 __global__ __launch_bounds__(kCombWaves * 64) void k_attn_combine(AttnArgs a) {
     __shared__ CombState xs[kCombWaves][64];
-    const int hq = blockIdx.x >> 3, dt = blockIdx.x & 7;
+    // the same XCD placement as the split kernel: the workgroups of query
+    // head hq run on the XCD that wrote its partials
+    int hq, dt;
+    if ((a.Hkv & 7) == 0) {
+        const int rest = blockIdx.x >> 3, t2 = rest >> 3, kvl = t2 / a.G;
+        dt = rest & 7;
+        hq = ((blockIdx.x & 7) + 8 * kvl) * a.G + (t2 - kvl * a.G);
+    } else {
+        hq = blockIdx.x >> 3;
+        dt = blockIdx.x & 7;
+    }
     const int lane = threadIdx.x & 63, sg = threadIdx.x >> 6;
     const int r = lane & 15, g = lane >> 4;
     const float2 *ml = (const float2 *)a.ws_ml + (size_t)hq * a.S * 16 + r;          // + 16 s

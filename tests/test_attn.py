@@ -73,6 +73,7 @@ def check(q, k, v, T, W, splits=0, what=""):
     (24, 8, 16, 500, 100),      # G = 3: one wave of the workgroup has no head
     (16, 2, 16, 700, 300),      # G = 8: two heads per wave
     (12, 2, 16, 333, 64),       # G = 6: the second head exists for two waves only
+    (32, 16, 16, 300, 64),      # 16 key/value heads: two per XCD
     (8, 2, 5, 400, 128),        # ragged block: 5 queries
     (2, 1, 1, 1, 0),            # one token
     (2, 1, 16, 16, 0),          # cache = the block
