@@ -58,10 +58,13 @@ static_assert((kWaves & (kWaves - 1)) == 0, "waves per workgroup must be a power
 // TILED kernel (prefill-sized M): a workgroup of kTiledWaves waves computes
 // kTiledBM rows x kTiledBN columns; wave (wm, wn) owns kTiledNT column tiles
 // and kTiledMSW m-subtiles of 16 rows.
-constexpr int kTiledWaves = 8;
+#ifndef QLIN_TILED_WAVES
+#define QLIN_TILED_WAVES 4
+#endif
+constexpr int kTiledWaves = QLIN_TILED_WAVES;              // 4: one wave per tile set (8: two, sharing it)
 constexpr int kTiledNT = 4;
 constexpr int kTiledBM = 128;
-constexpr int kTiledMSW = kTiledBM / 16 / 2;               // 4: two waves per tile set
+constexpr int kTiledMSW = kTiledBM / 16 / (kTiledWaves / 4);   // m-subtiles of 16 rows per wave
 constexpr int kTiledBN = 4 * kTiledNT * kTileN;            // 256 columns
 constexpr int kTiledXLoads = kTiledBM * 16 / (kTiledWaves * 64);   // direct-to-LDS loads per wave and group
 constexpr int kTiledStages = 3;                            // LDS pipeline depth (groups)

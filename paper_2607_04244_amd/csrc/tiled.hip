@@ -38,7 +38,7 @@ namespace qlin {
 // tile and are not written.
 
 template <bool SYM>
-__global__ void __launch_bounds__(kTiledWaves * 64, 2) k_tiled(TiledArgs a) {
+__global__ void __launch_bounds__(kTiledWaves * 64, 8 / kTiledWaves) k_tiled(TiledArgs a) {
     constexpr int kTiles = kTiledBN / kTileN;            // 16 tiles per workgroup
     __shared__ __align__(16) uint4 xs[kTiledStages][kTiledBM * 16];
     // the workgroup's 16 weight blocks (1 KiB each) and their s|z words (64
@@ -70,11 +70,14 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 2) k_tiled(TiledArgs a) {
         const int row = min(im * kTiledBM + r, a.M - 1);
         xo[i] = (uint32_t)row * (uint32_t)a.K + (uint32_t)(((lane & 15) ^ (r & 15)) * 8);
     }
+    // All global reads are direct-to-LDS loads issued through inline assembly
+    // (load_lds_x16 / load_lds_x4): the compiler does not track them, so the
+    // only waits are the explicit vmcnt below and the pipeline keeps S - 1
+    // groups in flight across the barriers.
     auto load_x = [&](int kb, int buf) {
 #pragma unroll
         for (int i = 0; i < kTiledXLoads; ++i)
-            __builtin_amdgcn_global_load_lds((glb_void_t *)(a.x + xo[i] + (uint32_t)kb * kGroup),
-                                             (lds_void_t *)&xs[buf][(wave * kRowsPerWave + 4 * i) * 16], 16, 0, 0);
+            load_lds_x16(a.x + xo[i] + (uint32_t)kb * kGroup, &xs[buf][(wave * kRowsPerWave + 4 * i) * 16]);
     };
     // weights: wave (wm, wn) loads tiles 4 wn + 2 wm + u, u < 2 (clamped to
     // the last tile); wo = uint4 index of block (tile, 0) / 64
@@ -88,16 +91,13 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 2) k_tiled(TiledArgs a) {
         for (int u = 0; u < kWLoads; ++u) {
             const uint32_t b = wo[u] + (uint32_t)kb;
             const int slot = (wn * kTiledNT + kWLoads * wm + u) * 64;
-            __builtin_amdgcn_global_load_lds((glb_void_t *)(a.codes + (size_t)b * 64 + lane),
-                                             (lds_void_t *)&ws_codes[buf][slot], 16, 0, 0);
+            load_lds_x16(a.codes + (size_t)b * 64 + lane, &ws_codes[buf][slot]);
             if constexpr (SYM) {
                 // 2-byte scales: one dword per lane covers columns 2i, 2i + 1;
                 // read_w picks the half
-                __builtin_amdgcn_global_load_lds((glb_void_t *)((const uint32_t *)a.sz + (size_t)b * (kTileN / 2) + (lane & 7)),
-                                                 (lds_void_t *)&ws_sz[buf][slot], 4, 0, 0);
+                load_lds_x4((const uint32_t *)a.sz + (size_t)b * (kTileN / 2) + (lane & 7), &ws_sz[buf][slot]);
             } else {
-                __builtin_amdgcn_global_load_lds((glb_void_t *)((const uint32_t *)a.sz + (size_t)b * kTileN + lm),
-                                                 (lds_void_t *)&ws_sz[buf][slot], 4, 0, 0);
+                load_lds_x4((const uint32_t *)a.sz + (size_t)b * kTileN + lm, &ws_sz[buf][slot]);
             }
         }
     };
@@ -168,9 +168,9 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 2) k_tiled(TiledArgs a) {
         load_x(min(kb + S - 1, a.Kb - 1), nb);
         load_w(min(kb + S - 1, a.Kb - 1), nb);
         asm volatile("s_waitcnt vmcnt(%0)" :: "n"((S - 1) * kIssued) : "memory");
-        __syncthreads();                      // group kb is in LDS for every wave
+        lds_barrier();                        // group kb is in LDS for every wave
         compute(buf);
-        __syncthreads();                      // everyone is done reading buf before it is refilled
+        lds_barrier();                        // everyone is done reading buf before it is refilled
         buf = buf == S - 1 ? 0 : buf + 1;
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the reloads past the end
