@@ -117,13 +117,18 @@ def cpu_baseline(case, budget_s=12.0):
 
 
 def graph_time_us(torch, stream, launches, reps):
-    """Capture `launches` (list of callables) in one graph; median us per launch."""
+    """Capture `launches` (list of callables) in one graph; mean us per launch
+    over `reps` replays (at least 5) after 3 untimed ones: the first replays
+    after a capture run slower (clocks and caches still settling), by up to
+    a third for a graph of a few milliseconds."""
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=stream):
         for f in launches:
             f()
-    g.replay()
+    for _ in range(3):
+        g.replay()
     stream.synchronize()
+    reps = max(reps, 5)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     with torch.cuda.stream(stream):

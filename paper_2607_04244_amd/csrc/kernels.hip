@@ -365,13 +365,20 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     const DiagSel dsel(lane);
 
     // 1) the x chunk, straight into LDS: load i fills slots [64 i, 64 i + 64)
-    //    (the last one may run past the chunk into spare LDS)
+    //    (the last one may run past the chunk into spare LDS).  The row of a
+    //    slot is a quotient by the row pitch d = n8 + 1, taken as the high word
+    //    of sl * ceil(2^32 / d): exact because sl and d stay below 2^16 (the
+    //    staged chunk fits in LDS), and a generic 32-bit division would cost
+    //    a dozen vector instructions per load.
+    const uint32_t d = (uint32_t)n8 + 1u;
+    const uint32_t inv_d = 0xFFFFFFFFu / d + 1u;
+    const uint16_t *xg = a.x + (size_t)w.g0 * kGroup;
     for (int i = wave; i < nload; i += kWaves) {
-        const int sl = i * 64 + lane;
-        const int r = sl / (n8 + 1);                  // row; q8 == n8 is the pad slot
-        const int q8 = min(sl - r * (n8 + 1), n8 - 1);
-        const int row = min(r, a.M - 1);
-        load_lds_x16(a.x + (size_t)row * a.K + (size_t)w.g0 * kGroup + q8 * 8, xs + i * 64);
+        const uint32_t sl = (uint32_t)(i * 64 + lane);
+        const uint32_t r = __umulhi(sl, inv_d);      // row; q8 == n8 is the pad slot
+        const uint32_t q8 = min(sl - r * d, (uint32_t)n8 - 1u);
+        const uint32_t row = min(r, (uint32_t)a.M - 1u);
+        load_lds_x16(xg + (row * (uint32_t)a.K + q8 * 8u), xs + i * 64);
     }
     // 2) then the first weight blocks (younger than the x loads, so waiting
     //    for x below does not wait for them).  A wave with an empty range
@@ -894,7 +901,7 @@ static FwdKernel pick_kernel(int kern, int mrows, int tn, bool symmetric) {
 
 const char *kernel_name(int kern, int mrows, int tn, bool symmetric) {
     static thread_local char buf[64];
-    if (kern == kKernTiled) snprintf(buf, sizeof buf, "k_tiled%s", symmetric ? "<sym>" : "");
+    if (kern == kKernTiled) snprintf(buf, sizeof buf, "k_tiled<%d,%d%s>", mrows / 16, tn, symmetric ? ",sym" : "");
     else if (kern == kKernMfma16) snprintf(buf, sizeof buf, "k_mfma16<%d%s>", tn, symmetric ? ",sym" : "");
     else if (kern == kKernGemv) snprintf(buf, sizeof buf, "k_gemv4<%d,%d%s>", mrows, tn, symmetric ? ",sym" : "");
     else snprintf(buf, sizeof buf, "k_skinny<%d,%d%s>", mrows / 16, tn, symmetric ? ",sym" : "");

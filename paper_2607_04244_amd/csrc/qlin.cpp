@@ -282,19 +282,33 @@ double plan_cost(const qlin_s *h, int kern, int M, int S, int Gn) {
     return t;
 }
 
-// TILED plan: one launch over all M rows, 128 x 256 output blocks, grid
-// padded to a multiple of 8 column blocks (see k_tiled).
+// TILED plan: one launch over all M rows.  Block shape 128 x 256 when its
+// blocks fill the last round of compute units at least 60% (each unit runs
+// one such block at a time), else 64 x 128 (two per unit): measured on
+// MI355X over the decoder's linears at M = 128 .. 2048, the large block is
+// up to 20% faster per flop once the units are busy, and narrow layers at
+// small M lose up to 2x with it.  The grid is padded to a multiple of 8
+// column blocks (see k_tiled).
 int make_tiled_plan(const qlin_s *h, int64_t split_k, int64_t M, Plan *p) {
     if (split_k > 1) return fail(QLIN_ERR_UNSUPPORTED, "split_k=%d does not fit (TILED path runs the whole K range)", (int)split_k);
     if (M * h->K >= ((int64_t)1 << 31)) return fail(QLIN_ERR_UNSUPPORTED, "TILED path needs M * K < 2^31");
-    const int Mt = (int)((M + kTiledBM - 1) / kTiledBM);
-    const int Gn = (h->Nt + 15) / 16;
+    const TiledShape big = kTiledShapes[0], small = kTiledShapes[1];
+    const int64_t blocks = ((M + 16 * big.msw - 1) / (16 * big.msw)) * ((h->Nt + 4 * big.nt - 1) / (4 * big.nt));
+    const int64_t rounds = (blocks + h->num_cu - 1) / h->num_cu;
+    TiledShape sh = (blocks * 10 >= rounds * h->num_cu * 6) ? big : small;
+    static const int forced = [] {                   // tuning knob: QLIN_TILED_SHAPE = index into kTiledShapes
+        const char *e = getenv("QLIN_TILED_SHAPE");
+        return e ? atoi(e) : -1;
+    }();
+    if (forced >= 0 && forced < (int)(sizeof kTiledShapes / sizeof kTiledShapes[0])) sh = kTiledShapes[forced];
+    const int Mt = (int)((M + 16 * sh.msw - 1) / (16 * sh.msw));
+    const int Gn = (h->Nt + 4 * sh.nt - 1) / (4 * sh.nt);
     p->path = kTiled;
     p->kern = kKernTiled;
-    p->mrows = kTiledBM;
+    p->mrows = 16 * sh.msw;
     p->S = 1;
     p->Gn = Gn;
-    p->tn = 0;
+    p->tn = sh.nt;
     p->grid = 8 * ((Gn + 7) / 8) * Mt;
     p->lds = 0;
     return QLIN_OK;
@@ -302,13 +316,13 @@ int make_tiled_plan(const qlin_s *h, int64_t split_k, int64_t M, Plan *p) {
 
 // Does the automatic choice run M rows through the TILED kernel (one
 // launch) rather than 64-row slices of the decode kernels?  Measured on
-// MI355X: the tiled kernel wins once it has enough output blocks to spread
-// (about 64, or 16 from M = 256 on); narrow layers at M = 128 (k, v, o, down)
-// are faster as two slices.
+// MI355X: from M = 256 on the tiled kernel always wins; at M = 128 it wins
+// once it has about 64 blocks of 64 x 128 (q|k|v, gate|up), and the narrow
+// layers (o, down: 40 blocks) are faster as two slices.
 bool auto_tiled(const qlin_s *h, int64_t M) {
     if (M <= kMaxSkinnyM) return false;
-    const int64_t blocks = ((M + kTiledBM - 1) / kTiledBM) * ((h->Nt + 15) / 16);
-    return blocks >= 64 || (M >= 256 && blocks >= 16);
+    const int64_t blocks = ((M + 63) / 64) * ((h->Nt + 7) / 8);      // 64 x 128 blocks
+    return M >= 256 || blocks >= 64;
 }
 
 int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
@@ -423,9 +437,9 @@ int run_forward(qlin_s *h, int path, int64_t split_k, int64_t M, const uint16_t 
         a.N = (int)h->N;
         a.Kb = h->Kb;
         a.Nt = h->Nt;
-        a.Mt = (int)((M + kTiledBM - 1) / kTiledBM);
+        a.Mt = (int)((M + p.mrows - 1) / p.mrows);
         a.Gn = p.Gn;
-        e = launch_tiled(h->symmetric, a, p.grid, st);
+        e = launch_tiled(h->symmetric, TiledShape{p.mrows / 16, p.tn}, a, p.grid, st);
         if (e != hipSuccess) return hip_fail(e, "tiled launch");
         return QLIN_OK;
     }

@@ -55,19 +55,15 @@ struct FwdArgs {
 };
 static_assert((kWaves & (kWaves - 1)) == 0, "waves per workgroup must be a power of two");
 
-// TILED kernel (prefill-sized M): a workgroup of kTiledWaves waves computes
-// kTiledBM rows x kTiledBN columns; wave (wm, wn) owns kTiledNT column tiles
-// and kTiledMSW m-subtiles of 16 rows.
-#ifndef QLIN_TILED_WAVES
-#define QLIN_TILED_WAVES 4
-#endif
-constexpr int kTiledWaves = QLIN_TILED_WAVES;              // 4: one wave per tile set (8: two, sharing it)
-constexpr int kTiledNT = 4;
-constexpr int kTiledBM = 128;
-constexpr int kTiledMSW = kTiledBM / 16 / (kTiledWaves / 4);   // m-subtiles of 16 rows per wave
-constexpr int kTiledBN = 4 * kTiledNT * kTileN;            // 256 columns
-constexpr int kTiledXLoads = kTiledBM * 16 / (kTiledWaves * 64);   // direct-to-LDS loads per wave and group
+// TILED kernel (prefill-sized M): a workgroup of kTiledWaves = 4 waves
+// computes a (16 MSW) x (64 NT) block of y; wave w owns all 16 MSW rows of
+// column tiles NT w .. NT w + NT - 1.  Block shapes (MSW, NT): 128 x 256
+// (8, 4), 128 x 128 (8, 2) and 64 x 128 (4, 2); the planner takes the
+// largest that still gives every compute unit a block.
+constexpr int kTiledWaves = 4;
 constexpr int kTiledStages = 3;                            // LDS pipeline depth (groups)
+struct TiledShape { int msw, nt; };
+constexpr TiledShape kTiledShapes[] = {{8, 4}, {4, 2}};
 
 struct TiledArgs {
     const uint4 *codes;
@@ -75,8 +71,8 @@ struct TiledArgs {
     const uint16_t *x;
     uint16_t *y;
     int M, K, N, Kb, Nt;
-    int Mt;                 // row blocks: ceil(M / kTiledBM)
-    int Gn;                 // column blocks: ceil(Nt / 16)
+    int Mt;                 // row blocks: ceil(M / (16 MSW))
+    int Gn;                 // column blocks: ceil(Nt / (4 NT))
 };
 
 // Rows of x a SKINNY workgroup keeps in LDS for M rows (M <= 64): the next
@@ -115,7 +111,7 @@ hipError_t launch_dequant(int routine, const uint4 *codes, const void *sz, bool 
 hipError_t prepare_kernels();     // per-process attribute setup (LDS limits)
 hipError_t launch_quantize(const uint16_t *w, const uint16_t *scales, const uint16_t *zeros, uint32_t *packed,
                            int K, int N, hipStream_t st);
-hipError_t launch_tiled(bool symmetric, const TiledArgs &a, int grid, hipStream_t st);
+hipError_t launch_tiled(bool symmetric, TiledShape shape, const TiledArgs &a, int grid, hipStream_t st);
 hipError_t launch_stream_read(const void *buf, size_t bytes, int grid, uint32_t *sink, hipStream_t st);
 const char *kernel_name(int kern, int mrows, int tn, bool symmetric);
 

@@ -13,17 +13,15 @@ namespace qlin {
 
 // ---- TILED: prefill-sized M (GEMM), matrix-core dequantization ----------
 //
-// A workgroup of kTiledWaves = 8 waves computes a kTiledBM x kTiledBN = 128 x
-// 256 block of y: rows [128 im, 128 im + 128), column tiles [16 jn, 16 jn +
-// 16).  Wave (wm, wn) = (w >> 2, w & 3) owns rows [64 wm, 64 wm + 64) (four
-// m-subtiles of 16) of the four tiles 4 wn + t, t < 4: two waves share each
-// tile set and sit on one SIMD, so while one dequantizes (vector ALU) the
-// other's matrix products run.  Per group kb the workgroup stages the
-// 128 x 128 x-tile and the 16 weight blocks (plus their scales) in LDS with
-// direct-to-LDS loads (global_load_lds, no VGPR round trip), kTiledStages
-// groups deep.  Dequantization (the matrix-core route) produces the A
-// operand of v_mfma_f32_16x16x32_bf16 directly; each x fragment read from
-// LDS feeds the four tiles of the wave.
+// A workgroup of kTiledWaves = 4 waves computes a BM x BN = 16 MSW x 64 NT
+// block of y: rows [BM im, BM im + BM), column tiles [4 NT jn, 4 NT jn + 4 NT).
+// Wave w owns all BM rows (MSW m-subtiles of 16) of the NT tiles NT w + t:
+// each tile is dequantized once per workgroup and every dequantized operand
+// feeds MSW matrix products.  Per group kb the workgroup stages the BM x 128
+// x-tile and its 4 NT weight blocks (plus their scales) in LDS with
+// direct-to-LDS loads, kTiledStages groups deep.  Dequantization (the
+// matrix-core route) produces the A operand of v_mfma_f32_16x16x32_bf16
+// directly; each x fragment read from LDS feeds the NT tiles of the wave.
 //
 // x tile in LDS: 16-byte chunk (row r, c) = x[row][128 kb + 8c .. + 8],
 // c < 16, at slot 16 r + (c ^ (r & 15)): a wave's direct-to-LDS load fills 64
@@ -37,18 +35,20 @@ namespace qlin {
 // by the row blocks.  Rows >= M and tiles >= Nt load a clamped valid row or
 // tile and are not written.
 
-template <bool SYM>
-__global__ void __launch_bounds__(kTiledWaves * 64, 8 / kTiledWaves) k_tiled(TiledArgs a) {
-    constexpr int kTiles = kTiledBN / kTileN;            // 16 tiles per workgroup
-    __shared__ __align__(16) uint4 xs[kTiledStages][kTiledBM * 16];
-    // the workgroup's 16 weight blocks (1 KiB each) and their s|z words (64
-    // per tile: lane l of a load writes the word of column l & 15, the other
-    // 48 are copies), one buffer per pipeline stage
+template <bool SYM, int MSW, int NT>
+__global__ void __launch_bounds__(kTiledWaves * 64, MSW * NT <= 8 ? 2 : 1) k_tiled(TiledArgs a) {
+    constexpr int BM = 16 * MSW;
+    constexpr int kTiles = kTiledWaves * NT;              // column tiles per workgroup
+    constexpr int kXLoads = BM * 16 / (kTiledWaves * 64); // direct-to-LDS x loads per wave and group
+    constexpr int kRowsPerWave = BM / kTiledWaves;
+    __shared__ __align__(16) uint4 xs[kTiledStages][BM * 16];
+    // the workgroup's weight blocks (1 KiB each) and their s|z words (64 per
+    // tile: lane l of a load writes the word of column l & 15, the other 48
+    // are copies), one buffer per pipeline stage
     __shared__ __align__(16) uint4 ws_codes[kTiledStages][kTiles * 64];
     __shared__ __align__(16) uint32_t ws_sz[kTiledStages][kTiles * 64];
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave >> 2, wn = wave & 3;
     const ExtractConsts kx;
     // block index -> (column block jn, row block im)
     const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3;
@@ -59,38 +59,35 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 8 / kTiledWaves) k_tiled(Til
     const int lm = lane & 15, lg = lane >> 4;
     const DiagSel dsel(lane);
 
-    // x: load i of wave w fills rows 16 w + 4 i + (lane >> 4), slot position
-    // lane & 15, which holds chunk (lane & 15) ^ (row & 15) of that row.
-    // Element offsets from x at group 0; the planner keeps M * K below 2^31.
-    constexpr int kRowsPerWave = kTiledBM / kTiledWaves;     // 16
-    uint32_t xo[kTiledXLoads];
+    // x: load i of wave w fills rows kRowsPerWave w + 4 i + (lane >> 4), slot
+    // position lane & 15, which holds chunk (lane & 15) ^ (row & 15) of that
+    // row.  Element offsets from x at group 0; the planner keeps M * K below 2^31.
+    uint32_t xo[kXLoads];
 #pragma unroll
-    for (int i = 0; i < kTiledXLoads; ++i) {
+    for (int i = 0; i < kXLoads; ++i) {
         const int r = wave * kRowsPerWave + 4 * i + lg;
-        const int row = min(im * kTiledBM + r, a.M - 1);
+        const int row = min(im * BM + r, a.M - 1);
         xo[i] = (uint32_t)row * (uint32_t)a.K + (uint32_t)(((lane & 15) ^ (r & 15)) * 8);
     }
     // All global reads are direct-to-LDS loads issued through inline assembly
     // (load_lds_x16 / load_lds_x4): the compiler does not track them, so the
-    // only waits are the explicit vmcnt below and the pipeline keeps S - 1
-    // groups in flight across the barriers.
+    // only waits are the explicit vmcnt below and the pipeline keeps
+    // kTiledStages - 1 groups in flight across the barriers.
     auto load_x = [&](int kb, int buf) {
 #pragma unroll
-        for (int i = 0; i < kTiledXLoads; ++i)
+        for (int i = 0; i < kXLoads; ++i)
             load_lds_x16(a.x + xo[i] + (uint32_t)kb * kGroup, &xs[buf][(wave * kRowsPerWave + 4 * i) * 16]);
     };
-    // weights: wave (wm, wn) loads tiles 4 wn + 2 wm + u, u < 2 (clamped to
-    // the last tile); wo = uint4 index of block (tile, 0) / 64
-    constexpr int kWLoads = kTiles / kTiledWaves;            // 2 tiles per wave
-    uint32_t wo[kWLoads];
+    // weights: wave w loads its own tiles NT w + u (clamped to the last
+    // tile); wo = uint4 index of block (tile, 0) / 64
+    uint32_t wo[NT];
 #pragma unroll
-    for (int u = 0; u < kWLoads; ++u)
-        wo[u] = (uint32_t)min(jn * kTiles + wn * kTiledNT + kWLoads * wm + u, a.Nt - 1) * (uint32_t)a.Kb;
+    for (int u = 0; u < NT; ++u) wo[u] = (uint32_t)min(jn * kTiles + wave * NT + u, a.Nt - 1) * (uint32_t)a.Kb;
     auto load_w = [&](int kb, int buf) {
 #pragma unroll
-        for (int u = 0; u < kWLoads; ++u) {
+        for (int u = 0; u < NT; ++u) {
             const uint32_t b = wo[u] + (uint32_t)kb;
-            const int slot = (wn * kTiledNT + kWLoads * wm + u) * 64;
+            const int slot = (wave * NT + u) * 64;
             load_lds_x16(a.codes + (size_t)b * 64 + lane, &ws_codes[buf][slot]);
             if constexpr (SYM) {
                 // 2-byte scales: one dword per lane covers columns 2i, 2i + 1;
@@ -102,10 +99,10 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 8 / kTiledWaves) k_tiled(Til
         }
     };
     // this lane's code words and s|z word of the wave's tile t from LDS
-    auto read_w = [&](int buf, uint4 (&cw)[kTiledNT], uint32_t (&sw)[kTiledNT]) {
+    auto read_w = [&](int buf, uint4 (&cw)[NT], uint32_t (&sw)[NT]) {
 #pragma unroll
-        for (int t = 0; t < kTiledNT; ++t) {
-            const int slot = (wn * kTiledNT + t) * 64;
+        for (int t = 0; t < NT; ++t) {
+            const int slot = (wave * NT + t) * 64;
             cw[t] = ws_codes[buf][slot + lane];
             if constexpr (SYM) {
                 const uint32_t pair = ws_sz[buf][slot + (lm >> 1)];
@@ -116,35 +113,35 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 8 / kTiledWaves) k_tiled(Til
         }
     };
 
-    v4f acc[kTiledMSW][kTiledNT];
+    v4f acc[MSW][NT];
 #pragma unroll
-    for (int ms = 0; ms < kTiledMSW; ++ms)
+    for (int ms = 0; ms < MSW; ++ms)
 #pragma unroll
-        for (int t = 0; t < kTiledNT; ++t) acc[ms][t] = v4f{0, 0, 0, 0};
+        for (int t = 0; t < NT; ++t) acc[ms][t] = v4f{0, 0, 0, 0};
 
-    // LDS slot of this lane's operand read: row 64 wm + 16 ms + lm, chunk 4 j + lg
-    auto xslot = [&](int ms, int j) { return (kTiledMSW * wm + ms) * 256 + lm * 16 + ((4 * j + lg) ^ lm); };
+    // LDS slot of this lane's operand read: row 16 ms + lm, chunk 4 j + lg
+    auto xslot = [&](int ms, int j) { return ms * 256 + lm * 16 + ((4 * j + lg) ^ lm); };
 
     auto compute = [&](int buf) {
-        uint4 cw[kTiledNT];
-        uint32_t sw[kTiledNT];
+        uint4 cw[NT];
+        uint32_t sw[NT];
         read_w(buf, cw, sw);
-        MfmaDeq d[kTiledNT];
+        MfmaDeq d[NT];
 #pragma unroll
-        for (int t = 0; t < kTiledNT; ++t) d[t] = mfma_setup(sw[t], dsel);
+        for (int t = 0; t < NT; ++t) d[t] = mfma_setup(sw[t], dsel);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            v8bf wa[kTiledNT];
+            v8bf wa[NT];
 #pragma unroll
-            for (int t = 0; t < kTiledNT; ++t) {
+            for (int t = 0; t < NT; ++t) {
                 const uint32_t P = j == 0 ? cw[t].x : j == 1 ? cw[t].y : j == 2 ? cw[t].z : cw[t].w;
                 wa[t] = mfma_dequant(P, d[t], kx);
             }
 #pragma unroll
-            for (int ms = 0; ms < kTiledMSW; ++ms) {
+            for (int ms = 0; ms < MSW; ++ms) {
                 const v8bf xf = __builtin_bit_cast(v8bf, xs[buf][xslot(ms, j)]);
 #pragma unroll
-                for (int t = 0; t < kTiledNT; ++t)
+                for (int t = 0; t < NT; ++t)
                     acc[ms][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[t], xf, acc[ms][t], 0, 0, 0);
             }
         }
@@ -155,7 +152,7 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 8 / kTiledWaves) k_tiled(Til
     // issues one group's loads (kIssued memory instructions per wave; past
     // the last group they reload it into a buffer nobody reads), waits for
     // group kb's, and computes it.
-    constexpr int kIssued = kTiledXLoads + 2 * kWLoads;
+    constexpr int kIssued = kXLoads + 2 * NT;
     constexpr int S = kTiledStages;
 #pragma unroll
     for (int i = 0; i < S - 1; ++i) {
@@ -177,12 +174,12 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 8 / kTiledWaves) k_tiled(Til
 
     // D of the 16x16 op: lane l holds rows n = 4 (l >> 4) + v of column m = l & 15
 #pragma unroll
-    for (int ms = 0; ms < kTiledMSW; ++ms) {
-        const int row = im * kTiledBM + (kTiledMSW * wm + ms) * 16 + lm;
+    for (int ms = 0; ms < MSW; ++ms) {
+        const int row = im * BM + ms * 16 + lm;
         if (row >= a.M) continue;
 #pragma unroll
-        for (int t = 0; t < kTiledNT; ++t) {
-            const int tt = jn * kTiles + wn * kTiledNT + t;
+        for (int t = 0; t < NT; ++t) {
+            const int tt = jn * kTiles + wave * NT + t;
             if (tt >= a.Nt) continue;
             const v4f v = acc[ms][t];
             const uint2 o = make_uint2(cvt_pk_bf16(v[0], v[1]), cvt_pk_bf16(v[2], v[3]));
@@ -191,10 +188,17 @@ __global__ void __launch_bounds__(kTiledWaves * 64, 8 / kTiledWaves) k_tiled(Til
     }
 }
 
-hipError_t launch_tiled(bool symmetric, const TiledArgs &a, int grid, hipStream_t st) {
-    if (symmetric) hipLaunchKernelGGL(k_tiled<true>, dim3(grid), dim3(kTiledWaves * 64), 0, st, a);
-    else hipLaunchKernelGGL(k_tiled<false>, dim3(grid), dim3(kTiledWaves * 64), 0, st, a);
+template <bool SYM>
+hipError_t launch_tiled_sym(TiledShape sh, const TiledArgs &a, int grid, hipStream_t st) {
+    const dim3 g(grid), b(kTiledWaves * 64);
+    if (sh.msw == 8 && sh.nt == 4) hipLaunchKernelGGL((k_tiled<SYM, 8, 4>), g, b, 0, st, a);
+    else if (sh.msw == 4 && sh.nt == 2) hipLaunchKernelGGL((k_tiled<SYM, 4, 2>), g, b, 0, st, a);
+    else return hipErrorInvalidValue;
     return hipGetLastError();
+}
+
+hipError_t launch_tiled(bool symmetric, TiledShape shape, const TiledArgs &a, int grid, hipStream_t st) {
+    return symmetric ? launch_tiled_sym<true>(shape, a, grid, st) : launch_tiled_sym<false>(shape, a, grid, st);
 }
 
 }  // namespace qlin

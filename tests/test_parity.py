@@ -203,6 +203,22 @@ def test_tiled_matches_oracle(M, K, N):
     lin.close()
 
 
+@pytest.mark.parametrize("M,K,N,shape", [
+    (2100, 256, 16384, "k_tiled<8,4>"),     # 128 x 256 blocks: enough of them for every compute unit
+    (1500, 256, 8208, "k_tiled<8,4>"),      # 128 x 256 blocks, partial row and column blocks
+    (1000, 384, 4112, "k_tiled<4,2>"),      # 64 x 128 blocks, partial row and column blocks
+    (300, 640, 2576, "k_tiled<4,2>"),       # 64 x 128 blocks for a narrow layer
+])
+def test_tiled_block_shapes_match_oracle(M, K, N, shape):
+    """Each block shape of the prefill kernel, as the planner picks it,
+    every output compared."""
+    c = gen.random_case(M + K + N, M, K, N, sigma=1.0)
+    lin = make(c)
+    assert f"kernel={shape}" in lin.plan(M, TILED)
+    assert_close(run(lin, c["x"], TILED), oracle(c), f"{shape} M={M} K={K} N={N}")
+    lin.close()
+
+
 def test_tiled_integer_case_is_bit_exact():
     K, N, M = 1024, 272, 130
     rng = np.random.default_rng(5)
