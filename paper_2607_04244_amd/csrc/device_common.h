@@ -84,6 +84,21 @@ __device__ inline uint32_t load_sz(const void *sz, size_t idx) {
     }
 }
 
+// The same two loads for block b (wave-uniform) and lane l: the block's base
+// address is formed once in scalar registers, so each load is a scalar base
+// plus the lane's 32-bit offset, with no 64-bit vector address arithmetic.
+__device__ inline uint4 load_block_at(const uint4 *codes, uint32_t b, int lane) {
+    return (codes + (size_t)b * 64)[lane];
+}
+template <bool SYM>
+__device__ inline uint32_t load_sz_at(const void *sz, uint32_t b, int col) {
+    if constexpr (SYM) {
+        return (uint32_t)((const uint16_t *)sz + (size_t)b * 16)[col] | (kZcSymmetric << 16);
+    } else {
+        return ((const uint32_t *)sz + (size_t)b * 16)[col];
+    }
+}
+
 __device__ inline float dot2(uint32_t a, uint32_t b, float c) {
     return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(v2bf, a), __builtin_bit_cast(v2bf, b), c, false);
 }

@@ -181,25 +181,6 @@ __device__ inline void wave_range(int U, int i, int &u0, int &u1) {
     u1 = u0 + q + (i < r ? 1 : 0);
 }
 
-// Walks the blocks of a wave's range in tile-major order u = tl * Kc + kbl:
-// block index (t0 + tl) * Kb + g0 + kbl (consecutive blocks of a tile are
-// adjacent in memory) and position (tile tl, group kbl) within the
-// workgroup's work, no division.
-struct BlockWalk {
-    int tl, kbl;
-    size_t b;
-    __device__ inline void start(const WgWork &w, int Kb, int u) {
-        tl = 0;
-        kbl = u;
-        while (kbl >= w.Kc) { kbl -= w.Kc; ++tl; }   // u < Tn * Kc: at most Tn steps, once
-        b = (size_t)(w.t0 + tl) * Kb + w.g0 + kbl;
-    }
-    __device__ inline void next(const WgWork &w, int Kb) {
-        if (++kbl == w.Kc) { kbl = 0; ++tl; b += (size_t)(Kb - w.Kc) + 1; }
-        else ++b;
-    }
-};
-
 // Split-K partial sums travel between workgroups that may sit on different
 // XCDs, whose L2 caches are not coherent with each other for ordinary
 // accesses.  They are written and read with agent-scope (sc1) buffer
@@ -210,9 +191,10 @@ struct BlockWalk {
 // item it = (tile * M + m) * 2 + half at float offset 8 * it, so the 16-byte
 // accesses of a wave are contiguous.
 constexpr int kSc1 = 16;   // cache-policy operand of the buffer builtins: sc1 (agent scope)
+constexpr int kRsrcFlags = 0x00020000;   // buffer descriptor word 3: 32-bit raw data
 
 __device__ inline __amdgpu_buffer_rsrc_t ws_rsrc(const FwdArgs &a) {
-    return __builtin_amdgcn_make_buffer_rsrc(a.ws, 0, (int)a.ws_bytes, 0x00020000);
+    return __builtin_amdgcn_make_buffer_rsrc(a.ws, 0, (int)a.ws_bytes, kRsrcFlags);
 }
 __device__ inline uint32_t ws_region(const FwdArgs &a, int c, int jn) {      // byte offset
     return (uint32_t)((c * a.Gn + jn) * a.TnMax * a.M) * 64u;
@@ -381,19 +363,45 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
         load_lds_x16(xg + (row * (uint32_t)a.K + q8 * 8u), xs + i * 64);
     }
     // 2) then the first weight blocks (younger than the x loads, so waiting
-    //    for x below does not wait for them).  A wave with an empty range
-    //    re-reads one block, which is harmless.
-    BlockWalk pw;                       // prefetch position
-    pw.start(w, a.Kb, min(u0, U - 1));
-    int up = u0;                        // block index pw points at
+    //    for x below does not wait for them).  Block u of the workgroup's
+    //    work (tile-major, u = tl Kc + kbl) is block base + u + tl (Kb - Kc)
+    //    of the device layout, with tl = u / Kc taken as a multiply-high by
+    //    ceil(2^32 / Kc) (exact: u and Kc stay below 2^16; Kc = 1, whose
+    //    reciprocal needs 33 bits, is taken apart).  All of it is
+    //    wave-uniform scalar arithmetic without branches.  Prefetches past
+    //    the wave's last block re-read that block (a wave with an empty
+    //    range re-reads one block of the workgroup), which is harmless.
+    //    The loads go through buffer resources based at the workgroup's first
+    //    block (its blocks span at most Tn Kb KiB, well inside the 32-bit
+    //    range), so the block offset is a scalar operand of the load.
+    const bool kc1 = w.Kc == 1;
+    const uint32_t inv_kc = kc1 ? 0u : 0xFFFFFFFFu / (uint32_t)w.Kc + 1u;
+    const uint32_t kc1_mask = kc1 ? 0xFFFFFFFFu : 0u;       // selects u itself when Kc == 1, without a branch
+    auto tile_of = [&](uint32_t u) { return __umulhi(u, inv_kc) + (u & kc1_mask); };
+    const size_t base = (size_t)w.t0 * a.Kb + w.g0;
+    const uint32_t skip = (uint32_t)(a.Kb - w.Kc);
+    const uint32_t ulast = (uint32_t)(u0 < u1 ? u1 - 1 : min(u0, U - 1));
+    constexpr int kSzBytes = SYM ? 2 : 4;
+    const int span = w.Tn * a.Kb;                      // blocks from base to past the workgroup's last
+    const __amdgpu_buffer_rsrc_t rcodes =
+        __builtin_amdgcn_make_buffer_rsrc((void *)(a.codes + base * 64), 0, span * 1024, kRsrcFlags);
+    const __amdgpu_buffer_rsrc_t rsz = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((const char *)a.sz + base * kTileN * kSzBytes), 0, span * kTileN * kSzBytes, kRsrcFlags);
     uint4 cb[kDepth];
     uint32_t sb[kDepth];
+    auto fetch = [&](int d, uint32_t u) {
+        u = min(u, ulast);
+        const uint32_t rb = u + tile_of(u) * skip;                // block relative to base
+        cb[d] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rcodes, lane * 16, rb * 1024, 0));
+        if constexpr (SYM) {
+            sb[d] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rsz, lm * 2, rb * (kTileN * 2), 0) |
+                    (kZcSymmetric << 16);
+        } else {
+            sb[d] = __builtin_amdgcn_raw_buffer_load_b32(rsz, lm * 4, rb * (kTileN * 4), 0);
+        }
+    };
 #pragma unroll
-    for (int d = 0; d < kDepth; ++d) {
-        cb[d] = load_block(a.codes, pw.b * 64 + lane);
-        sb[d] = load_sz<SYM>(a.sz, pw.b * kTileN + lm);
-        if (up + 1 < u1) { pw.next(w, a.Kb); ++up; }
-    }
+    for (int d = 0; d < kDepth; ++d) fetch(d, (uint32_t)(u0 + d));
     // 3) every wave's x loads have landed in LDS (only the weight prefetch,
     //    2 kDepth loads, may still be in flight)
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * kDepth) : "memory");
@@ -409,14 +417,14 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
         v4f acc[MT];
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[mt] = v4f{0, 0, 0, 0};
-        BlockWalk cw;                   // consume position
-        cw.start(w, a.Kb, u0);
 
-        auto consume = [&](int u, const uint4 &cq, uint32_t szw) {
+        auto consume = [&](uint32_t u, const uint4 &cq, uint32_t szw) {
+            const uint32_t tl = tile_of(u);
+            const uint32_t kbl = u - tl * (uint32_t)w.Kc;
             v8bf xf[MT][4];
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) {
-                const uint4 *xb = xs + cw.kbl * 16 + xoff[mt];
+                const uint4 *xb = xs + kbl * 16 + xoff[mt];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) xf[mt][j] = __builtin_bit_cast(v8bf, xb[4 * j]);
             }
@@ -429,30 +437,29 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
                 for (int mt = 0; mt < MT; ++mt)
                     acc[mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa, xf[mt][j], acc[mt], 0, 0, 0);
             }
-            if (cw.kbl == w.Kc - 1 || u == u1 - 1) {
+            // the tile's run in this wave ends here (rare: kept off the
+            // straight-line path)
+            if (__builtin_expect(kbl == (uint32_t)w.Kc - 1u || u == (uint32_t)u1 - 1u, 0)) {
                 // D of the 16x16 op: lane l holds rows n = 4(l >> 4) + v of column m = l & 15
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
-                    *(v4f *)(slots + ((size_t)(wave + cw.tl) * MR + 16 * mt + lm) * 16 + 4 * lg) = acc[mt];
+                    *(v4f *)(slots + ((size_t)(wave + tl) * MR + 16 * mt + lm) * 16 + 4 * lg) = acc[mt];
                     acc[mt] = v4f{0, 0, 0, 0};
                 }
             }
-            cw.next(w, a.Kb);
         };
 
         int u = u0;
         for (; u + kDepth <= u1; u += kDepth) {
 #pragma unroll
             for (int d = 0; d < kDepth; ++d) {
-                consume(u + d, cb[d], sb[d]);
-                cb[d] = load_block(a.codes, pw.b * 64 + lane);
-                sb[d] = load_sz<SYM>(a.sz, pw.b * kTileN + lm);
-                if (up + 1 < u1) { pw.next(w, a.Kb); ++up; }
+                consume((uint32_t)(u + d), cb[d], sb[d]);
+                fetch(d, (uint32_t)(u + d + kDepth));
             }
         }
 #pragma unroll
         for (int d = 0; d < kDepth; ++d)
-            if (u + d < u1) consume(u + d, cb[d], sb[d]);
+            if (u + d < u1) consume((uint32_t)(u + d), cb[d], sb[d]);
     }
     lds_barrier();
     write_out(a, w, slots, MR);

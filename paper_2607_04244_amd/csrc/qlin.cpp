@@ -353,6 +353,8 @@ int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
         if (Gn > h->counters_n || Tn > tn_max_of(kern)) return false;
         if (kern != kKernStaged) return lds_bytes_regs(rows_of(kern), Tn) <= kLdsMax;
         if (!chunk_fits(Mi, Kc)) return false;
+        if ((int64_t)Tn * Kc >= 65536) return false;   // the kernel's block walk divides u < 2^16 by Kc
+        if ((int64_t)Tn * h->Kb * 1024 >= ((int64_t)1 << 31)) return false;   // span of its buffer descriptors
         return lds_bytes(Mi, Kc, Tn) <= kLdsMax;
     };
     // column ranges for S chunks: about one workgroup per CU, but no range

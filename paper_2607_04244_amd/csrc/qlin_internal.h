@@ -58,8 +58,8 @@ static_assert((kWaves & (kWaves - 1)) == 0, "waves per workgroup must be a power
 // TILED kernel (prefill-sized M): a workgroup of kTiledWaves = 4 waves
 // computes a (16 MSW) x (64 NT) block of y; wave w owns all 16 MSW rows of
 // column tiles NT w .. NT w + NT - 1.  Block shapes (MSW, NT): 128 x 256
-// (8, 4), 128 x 128 (8, 2) and 64 x 128 (4, 2); the planner takes the
-// largest that still gives every compute unit a block.
+// (8, 4) and 64 x 128 (4, 2); the planner takes the large one when its
+// blocks fill the last round of compute units well.
 constexpr int kTiledWaves = 4;
 constexpr int kTiledStages = 3;                            // LDS pipeline depth (groups)
 struct TiledShape { int msw, nt; };
