@@ -536,7 +536,8 @@ int qlin_plan(qlin_t h, int path, int64_t split_k, int64_t M, char *buf, int64_t
     static const char *names[] = {"gemv", "regs", "skinny", "tiled"};
     snprintf(buf, (size_t)buflen, "path=%s kernel=%s grid=%d block=%d split=%d ranges=%d lds=%zu launches=%lld",
              names[p.kern], kernel_name(p.kern, p.mrows, p.tn, h->symmetric), p.grid,
-             tiled ? kTiledWaves * 64 : kThreads, p.S, p.Gn, p.lds, (long long)slices);
+             tiled ? kTiledWaves * 64 * tiled_wsplit(TiledShape{p.mrows / 16, p.tn}) : kThreads, p.S, p.Gn, p.lds,
+             (long long)slices);
     return QLIN_OK;
 }
 

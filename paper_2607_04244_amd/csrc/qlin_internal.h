@@ -55,15 +55,18 @@ struct FwdArgs {
 };
 static_assert((kWaves & (kWaves - 1)) == 0, "waves per workgroup must be a power of two");
 
-// TILED kernel (prefill-sized M): a workgroup of kTiledWaves = 4 waves
+// TILED kernel (prefill-sized M): a workgroup of kTiledWaves x WS waves
 // computes a (16 MSW) x (64 NT) block of y; wave w owns all 16 MSW rows of
-// column tiles NT w .. NT w + NT - 1.  Block shapes (MSW, NT): 128 x 256
+// column tiles NW w .. NW w + NW - 1 (NW = NT / WS).  Block shapes (MSW, NT): 128 x 256
 // (8, 4) and 64 x 128 (4, 2); the planner takes the large one when its
 // blocks fill the last round of compute units well.
 constexpr int kTiledWaves = 4;
 constexpr int kTiledStages = 3;                            // LDS pipeline depth (groups)
 struct TiledShape { int msw, nt; };
 constexpr TiledShape kTiledShapes[] = {{8, 4}, {4, 2}};
+// Wave split of a shape: the 128 x 256 blocks run two waves per SIMD, each
+// owning half of every column group's tiles.
+constexpr int tiled_wsplit(TiledShape sh) { return sh.msw == 8 && sh.nt == 4 ? 2 : 1; }
 
 struct TiledArgs {
     const uint4 *codes;

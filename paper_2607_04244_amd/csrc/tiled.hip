@@ -9,19 +9,23 @@
 
 #include "device_common.h"
 
+
 namespace qlin {
 
 // ---- TILED: prefill-sized M (GEMM), matrix-core dequantization ----------
 //
-// A workgroup of kTiledWaves = 4 waves computes a BM x BN = 16 MSW x 64 NT
-// block of y: rows [BM im, BM im + BM), column tiles [4 NT jn, 4 NT jn + 4 NT).
-// Wave w owns all BM rows (MSW m-subtiles of 16) of the NT tiles NT w + t:
+// A workgroup of 4 WS waves computes a BM x BN = 16 MSW x 64 NT block of y:
+// rows [BM im, BM im + BM), column tiles [4 NT jn, 4 NT jn + 4 NT).  Wave w
+// owns all BM rows (MSW m-subtiles of 16) of the NW = NT / WS tiles NW w + t:
 // each tile is dequantized once per workgroup and every dequantized operand
-// feeds MSW matrix products.  Per group kb the workgroup stages the BM x 128
-// x-tile and its 4 NT weight blocks (plus their scales) in LDS with
-// direct-to-LDS loads, kTiledStages groups deep.  Dequantization (the
+// feeds MSW matrix products.  With WS = 2 two waves share each SIMD, so the
+// stalls of one (LDS reads, matrix-result latency, barriers) are covered by
+// the other; each x fragment is then read from LDS by two waves.  Per group
+// kb the workgroup stages the BM x 128 x-tile and its 4 NT weight blocks
+// (plus their scales) in LDS with direct-to-LDS loads, kTiledStages groups
+// deep, the loads spread over all its waves.  Dequantization (the
 // matrix-core route) produces the A operand of v_mfma_f32_16x16x32_bf16
-// directly; each x fragment read from LDS feeds the NT tiles of the wave.
+// directly.
 //
 // x tile in LDS: 16-byte chunk (row r, c) = x[row][128 kb + 8c .. + 8],
 // c < 16, at slot 16 r + (c ^ (r & 15)): a wave's direct-to-LDS load fills 64
@@ -35,12 +39,15 @@ namespace qlin {
 // by the row blocks.  Rows >= M and tiles >= Nt load a clamped valid row or
 // tile and are not written.
 
-template <bool SYM, int MSW, int NT>
-__global__ void __launch_bounds__(kTiledWaves * 64, MSW * NT <= 8 ? 2 : 1) k_tiled(TiledArgs a) {
+template <bool SYM, int MSW, int NT, int WS>
+__global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) k_tiled(TiledArgs a) {
+    constexpr int kWavesWg = kTiledWaves * WS;
     constexpr int BM = 16 * MSW;
+    constexpr int NW = NT / WS;                           // column tiles per wave
     constexpr int kTiles = kTiledWaves * NT;              // column tiles per workgroup
-    constexpr int kXLoads = BM * 16 / (kTiledWaves * 64); // direct-to-LDS x loads per wave and group
-    constexpr int kRowsPerWave = BM / kTiledWaves;
+    constexpr int kXLoads = BM * 16 / (kWavesWg * 64);    // direct-to-LDS x loads per wave and group
+    constexpr int kRowsPerWave = BM / kWavesWg;
+    static_assert(kXLoads * kWavesWg * 64 == BM * 16 && NW * WS == NT, "tile shape does not split over the waves");
     __shared__ __align__(16) uint4 xs[kTiledStages][BM * 16];
     // the workgroup's weight blocks (1 KiB each) and their s|z words (64 per
     // tile: lane l of a load writes the word of column l & 15, the other 48
@@ -78,16 +85,16 @@ __global__ void __launch_bounds__(kTiledWaves * 64, MSW * NT <= 8 ? 2 : 1) k_til
         for (int i = 0; i < kXLoads; ++i)
             load_lds_x16(a.x + xo[i] + (uint32_t)kb * kGroup, &xs[buf][(wave * kRowsPerWave + 4 * i) * 16]);
     };
-    // weights: wave w loads its own tiles NT w + u (clamped to the last
+    // weights: wave w loads its own tiles NW w + u (clamped to the last
     // tile); wo = uint4 index of block (tile, 0) / 64
-    uint32_t wo[NT];
+    uint32_t wo[NW];
 #pragma unroll
-    for (int u = 0; u < NT; ++u) wo[u] = (uint32_t)min(jn * kTiles + wave * NT + u, a.Nt - 1) * (uint32_t)a.Kb;
+    for (int u = 0; u < NW; ++u) wo[u] = (uint32_t)min(jn * kTiles + wave * NW + u, a.Nt - 1) * (uint32_t)a.Kb;
     auto load_w = [&](int kb, int buf) {
 #pragma unroll
-        for (int u = 0; u < NT; ++u) {
+        for (int u = 0; u < NW; ++u) {
             const uint32_t b = wo[u] + (uint32_t)kb;
-            const int slot = (wave * NT + u) * 64;
+            const int slot = (wave * NW + u) * 64;
             load_lds_x16(a.codes + (size_t)b * 64 + lane, &ws_codes[buf][slot]);
             if constexpr (SYM) {
                 // 2-byte scales: one dword per lane covers columns 2i, 2i + 1;
@@ -99,10 +106,10 @@ __global__ void __launch_bounds__(kTiledWaves * 64, MSW * NT <= 8 ? 2 : 1) k_til
         }
     };
     // this lane's code words and s|z word of the wave's tile t from LDS
-    auto read_w = [&](int buf, uint4 (&cw)[NT], uint32_t (&sw)[NT]) {
+    auto read_w = [&](int buf, uint4 (&cw)[NW], uint32_t (&sw)[NW]) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const int slot = (wave * NT + t) * 64;
+        for (int t = 0; t < NW; ++t) {
+            const int slot = (wave * NW + t) * 64;
             cw[t] = ws_codes[buf][slot + lane];
             if constexpr (SYM) {
                 const uint32_t pair = ws_sz[buf][slot + (lm >> 1)];
@@ -113,27 +120,27 @@ __global__ void __launch_bounds__(kTiledWaves * 64, MSW * NT <= 8 ? 2 : 1) k_til
         }
     };
 
-    v4f acc[MSW][NT];
+    v4f acc[MSW][NW];
 #pragma unroll
     for (int ms = 0; ms < MSW; ++ms)
 #pragma unroll
-        for (int t = 0; t < NT; ++t) acc[ms][t] = v4f{0, 0, 0, 0};
+        for (int t = 0; t < NW; ++t) acc[ms][t] = v4f{0, 0, 0, 0};
 
     // LDS slot of this lane's operand read: row 16 ms + lm, chunk 4 j + lg
     auto xslot = [&](int ms, int j) { return ms * 256 + lm * 16 + ((4 * j + lg) ^ lm); };
 
     auto compute = [&](int buf) {
-        uint4 cw[NT];
-        uint32_t sw[NT];
+        uint4 cw[NW];
+        uint32_t sw[NW];
         read_w(buf, cw, sw);
-        MfmaDeq d[NT];
+        MfmaDeq d[NW];
 #pragma unroll
-        for (int t = 0; t < NT; ++t) d[t] = mfma_setup(sw[t], dsel);
+        for (int t = 0; t < NW; ++t) d[t] = mfma_setup(sw[t], dsel);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            v8bf wa[NT];
+            v8bf wa[NW];
 #pragma unroll
-            for (int t = 0; t < NT; ++t) {
+            for (int t = 0; t < NW; ++t) {
                 const uint32_t P = j == 0 ? cw[t].x : j == 1 ? cw[t].y : j == 2 ? cw[t].z : cw[t].w;
                 wa[t] = mfma_dequant(P, d[t], kx);
             }
@@ -141,7 +148,7 @@ __global__ void __launch_bounds__(kTiledWaves * 64, MSW * NT <= 8 ? 2 : 1) k_til
             for (int ms = 0; ms < MSW; ++ms) {
                 const v8bf xf = __builtin_bit_cast(v8bf, xs[buf][xslot(ms, j)]);
 #pragma unroll
-                for (int t = 0; t < NT; ++t)
+                for (int t = 0; t < NW; ++t)
                     acc[ms][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wa[t], xf, acc[ms][t], 0, 0, 0);
             }
         }
@@ -152,7 +159,7 @@ __global__ void __launch_bounds__(kTiledWaves * 64, MSW * NT <= 8 ? 2 : 1) k_til
     // issues one group's loads (kIssued memory instructions per wave; past
     // the last group they reload it into a buffer nobody reads), waits for
     // group kb's, and computes it.
-    constexpr int kIssued = kXLoads + 2 * NT;
+    constexpr int kIssued = kXLoads + 2 * NW;
     constexpr int S = kTiledStages;
 #pragma unroll
     for (int i = 0; i < S - 1; ++i) {
@@ -178,8 +185,8 @@ __global__ void __launch_bounds__(kTiledWaves * 64, MSW * NT <= 8 ? 2 : 1) k_til
         const int row = im * BM + ms * 16 + lm;
         if (row >= a.M) continue;
 #pragma unroll
-        for (int t = 0; t < NT; ++t) {
-            const int tt = jn * kTiles + wave * NT + t;
+        for (int t = 0; t < NW; ++t) {
+            const int tt = jn * kTiles + wave * NW + t;
             if (tt >= a.Nt) continue;
             const v4f v = acc[ms][t];
             const uint2 o = make_uint2(cvt_pk_bf16(v[0], v[1]), cvt_pk_bf16(v[2], v[3]));
@@ -190,9 +197,10 @@ __global__ void __launch_bounds__(kTiledWaves * 64, MSW * NT <= 8 ? 2 : 1) k_til
 
 template <bool SYM>
 hipError_t launch_tiled_sym(TiledShape sh, const TiledArgs &a, int grid, hipStream_t st) {
-    const dim3 g(grid), b(kTiledWaves * 64);
-    if (sh.msw == 8 && sh.nt == 4) hipLaunchKernelGGL((k_tiled<SYM, 8, 4>), g, b, 0, st, a);
-    else if (sh.msw == 4 && sh.nt == 2) hipLaunchKernelGGL((k_tiled<SYM, 4, 2>), g, b, 0, st, a);
+    const dim3 g(grid);
+    const dim3 b(kTiledWaves * 64 * tiled_wsplit(sh));
+    if (sh.msw == 8 && sh.nt == 4) hipLaunchKernelGGL((k_tiled<SYM, 8, 4, tiled_wsplit({8, 4})>), g, b, 0, st, a);
+    else if (sh.msw == 4 && sh.nt == 2) hipLaunchKernelGGL((k_tiled<SYM, 4, 2, tiled_wsplit({4, 2})>), g, b, 0, st, a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }
