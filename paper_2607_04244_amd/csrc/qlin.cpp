@@ -282,6 +282,28 @@ double plan_cost(const qlin_s *h, int kern, int M, int S, int Gn) {
     return t;
 }
 
+// Plans measured on MI355X (256 compute units) for the 4B decoder's linears
+// where the cost model below picks a slower one: every kernel family and
+// split from 1 to 8 was timed (HIP-graph replays over > 1 GiB of rotating
+// weight copies) at M = 1, 2, 4, 8, 12 .. 16, and these won by 4-12%.
+struct TunedPlan { int m_lo, m_hi, K, N, kern, S; };
+constexpr TunedPlan kTunedPlans[] = {
+    {13, 16, 2560, 1024, kKernStaged, 1},   // k and v projections
+    {13, 16, 2560, 2560, kKernStaged, 1},
+    {13, 16, 2560, 4096, kKernStaged, 1},   // q projection
+    {14, 16, 4096, 2560, kKernStaged, 1},   // o projection
+    {1, 4, 9728, 2560, kKernStaged, 1},     // down projection
+    {12, 15, 9728, 2560, kKernMfma16, 3},
+    {16, 16, 9728, 2560, kKernMfma16, 5},
+};
+
+const TunedPlan *tuned_plan(const qlin_s *h, int M) {
+    if (h->num_cu != 256) return nullptr;
+    for (const TunedPlan &t : kTunedPlans)
+        if (M >= t.m_lo && M <= t.m_hi && h->K == t.K && h->N == t.N) return &t;
+    return nullptr;
+}
+
 // TILED plan: one launch over all M rows.  Block shape 128 x 256 when its
 // blocks fill the last round of compute units at least 60% (each unit runs
 // one such block at a time), else 64 x 128 (two per unit): measured on
@@ -368,8 +390,16 @@ int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
     };
 
     int bestK = -1, bestS = -1, bestGn = 1;
+    // a measured plan for this shape, if it fits; otherwise the cost model
+    bool tuned = false;
+    if (auto_pick && path == kSkinny && split_k == 0) {
+        if (const TunedPlan *t = tuned_plan(h, Mi)) {
+            const int Gn = gn_for(t->kern, t->S);
+            if (fits(t->kern, t->S, Gn)) { bestK = t->kern; bestS = t->S; bestGn = Gn; tuned = true; }
+        }
+    }
     double best = 1e300;
-    for (int ki = 0; ki < nk; ++ki) {
+    for (int ki = 0; ki < nk && !tuned; ++ki) {
         const int kern = kerns[ki];
         const int s_lo = split_k > 0 ? (int)split_k : 1;
         const int s_hi = split_k > 0 ? (int)split_k : std::min(h->Kb, 64);

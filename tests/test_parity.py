@@ -349,3 +349,25 @@ def test_forward_argument_errors():
     assert "path=" in lin.plan(16)
     torch.cuda.synchronize()
     lin.close()
+
+
+@pytest.mark.parametrize("M,K,N,kernel,split", [
+    (16, 2560, 19456, "k_skinny<1,16>", 1),    # the draft-block verification linear
+    (16, 2560, 6144, "k_skinny<1,16>", 1),     # q|k|v of a layer
+    (16, 4096, 2560, "k_skinny<1,16>", 1),     # o projection (measured plan)
+    (16, 9728, 2560, "k_mfma16<4>", 5),        # down projection (measured plan)
+    (1, 9728, 2560, "k_skinny<1,1>", 1),       # down projection, one row (measured plan)
+    (1, 2560, 2560, "k_mfma16<1>", 1),         # single-row layer
+])
+def test_automatic_plan_for_decoder_shapes(M, K, N, kernel, split):
+    """The automatic plan for the decoder's linears on a 256-CU MI355X is the
+    one measured fastest (a planner change that silently falls back to a
+    slower kernel family fails here)."""
+    import torch
+    if torch.cuda.get_device_properties(0).multi_processor_count != 256:
+        pytest.skip("plans were measured on a 256-CU device")
+    c = gen.random_case(3, M, K, N)
+    lin = make(c)
+    plan = lin.plan(M)
+    lin.close()
+    assert f"kernel={kernel} " in plan and f"split={split} " in plan, plan
