@@ -117,27 +117,31 @@ def cpu_baseline(case, budget_s=12.0):
 
 
 def graph_time_us(torch, stream, launches, reps):
-    """Capture `launches` (list of callables) in one graph; mean us per launch
-    over `reps` replays (at least 5) after 3 untimed ones: the first replays
-    after a capture run slower (clocks and caches still settling), by up to
-    a third for a graph of a few milliseconds."""
+    """Capture `launches` (list of callables) in one graph; median us per launch
+    over `reps` replays (at least 5), each timed on its own (events around one
+    replay, then a synchronisation), after 3 untimed replays.  Every replay
+    runs on `stream`: a replay issued outside its context goes to the
+    default stream and overlaps the timed ones."""
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g, stream=stream):
         for f in launches:
             f()
-    for _ in range(3):
-        g.replay()
-    stream.synchronize()
-    reps = max(reps, 5)
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
     with torch.cuda.stream(stream):
-        ev0.record(stream)
-        for _ in range(reps):
+        for _ in range(3):
             g.replay()
-        ev1.record(stream)
-    stream.synchronize()
-    return ev0.elapsed_time(ev1) * 1e3 / (reps * len(launches)), g
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(max(reps, 5)):
+        ev0 = torch.cuda.Event(enable_timing=True)
+        ev1 = torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            ev0.record(stream)
+            g.replay()
+            ev1.record(stream)
+        stream.synchronize()
+        times.append(ev0.elapsed_time(ev1) * 1e3 / len(launches))
+    times.sort()
+    return times[len(times) // 2], g
 
 
 def stream_read_ceiling(torch, qlin, nbytes, stream):
@@ -384,8 +388,9 @@ def main():
     g_full = capture(R)
     tail = K_steps % R
     g_tail = capture(tail) if tail else None
-    for _ in range(2):
-        g_full.replay()
+    with torch.cuda.stream(stream):
+        for _ in range(2):
+            g_full.replay()
     stream.synchronize()
 
     ev0 = torch.cuda.Event(enable_timing=True)

@@ -304,20 +304,26 @@ const TunedPlan *tuned_plan(const qlin_s *h, int M) {
     return nullptr;
 }
 
-// TILED plan: one launch over all M rows.  Block shape 128 x 256 when its
-// blocks fill the last round of compute units at least 60% (each unit runs
-// one such block at a time), else 64 x 128 (two per unit): measured on
-// MI355X over the decoder's linears at M = 128 .. 2048, the large block is
-// up to 20% faster per flop once the units are busy, and narrow layers at
-// small M lose up to 2x with it.  The grid is padded to a multiple of 8
-// column blocks (see k_tiled).
+// TILED plan: one launch over all M rows.  The block shape minimises
+// (blocks per compute unit, rounded up) x (time of one block), with the
+// block times measured on MI355X relative to the 128 x 256 shape (same K):
+// 96 x 256 0.95, 64 x 128 0.42.  Ranked this way the three shapes come out
+// in the measured order for every decoder linear at M = 512 .. 2048 (or
+// within 2%): small blocks for narrow layers at small M, 96 x 256 where 128
+// rows would leave part of the chip idle, 128 x 256 otherwise.
 int make_tiled_plan(const qlin_s *h, int64_t split_k, int64_t M, Plan *p) {
     if (split_k > 1) return fail(QLIN_ERR_UNSUPPORTED, "split_k=%d does not fit (TILED path runs the whole K range)", (int)split_k);
     if (M * h->K >= ((int64_t)1 << 31)) return fail(QLIN_ERR_UNSUPPORTED, "TILED path needs M * K < 2^31");
-    const TiledShape big = kTiledShapes[0], small = kTiledShapes[1];
-    const int64_t blocks = ((M + 16 * big.msw - 1) / (16 * big.msw)) * ((h->Nt + 4 * big.nt - 1) / (4 * big.nt));
-    const int64_t rounds = (blocks + h->num_cu - 1) / h->num_cu;
-    TiledShape sh = (blocks * 10 >= rounds * h->num_cu * 6) ? big : small;
+    constexpr double kBlockTime[] = {1.0, 0.42, 0.95};           // per kTiledShapes entry
+    static_assert(sizeof kBlockTime / sizeof kBlockTime[0] == sizeof kTiledShapes / sizeof kTiledShapes[0], "");
+    TiledShape sh = kTiledShapes[0];
+    double best = 1e300;
+    for (int i = 0; i < (int)(sizeof kTiledShapes / sizeof kTiledShapes[0]); ++i) {
+        const TiledShape c = kTiledShapes[i];
+        const int64_t blocks = ((M + 16 * c.msw - 1) / (16 * c.msw)) * ((h->Nt + 4 * c.nt - 1) / (4 * c.nt));
+        const double t = (double)((blocks + h->num_cu - 1) / h->num_cu) * kBlockTime[i];
+        if (t < best) { best = t; sh = c; }
+    }
     static const int forced = [] {                   // tuning knob: QLIN_TILED_SHAPE = index into kTiledShapes
         const char *e = getenv("QLIN_TILED_SHAPE");
         return e ? atoi(e) : -1;
@@ -331,7 +337,7 @@ int make_tiled_plan(const qlin_s *h, int64_t split_k, int64_t M, Plan *p) {
     p->S = 1;
     p->Gn = Gn;
     p->tn = sh.nt;
-    p->grid = 8 * ((Gn + 7) / 8) * Mt;
+    p->grid = 8 * ((Gn * Mt + 7) / 8);
     p->lds = 0;
     return QLIN_OK;
 }

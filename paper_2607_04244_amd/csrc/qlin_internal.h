@@ -63,10 +63,10 @@ static_assert((kWaves & (kWaves - 1)) == 0, "waves per workgroup must be a power
 constexpr int kTiledWaves = 4;
 constexpr int kTiledStages = 3;                            // LDS pipeline depth (groups)
 struct TiledShape { int msw, nt; };
-constexpr TiledShape kTiledShapes[] = {{8, 4}, {4, 2}};
+constexpr TiledShape kTiledShapes[] = {{8, 4}, {4, 2}, {6, 4}};
 // Wave split of a shape: the 128 x 256 blocks run two waves per SIMD, each
 // owning half of every column group's tiles.
-constexpr int tiled_wsplit(TiledShape sh) { return sh.msw == 8 && sh.nt == 4 ? 2 : 1; }
+constexpr int tiled_wsplit(TiledShape sh) { return sh.nt == 4 ? 2 : 1; }
 
 struct TiledArgs {
     const uint4 *codes;

@@ -33,11 +33,12 @@ namespace qlin {
 // the global reads stay coalesced), and the operand reads (16 lanes = 16
 // rows of one c) hit 16 distinct bank groups.
 //
-// Workgroups sharing a column block are given block indices that are equal
-// modulo 8 (the XCD a workgroup runs on) and adjacent in dispatch order, so
-// the column block's weights are fetched once into that XCD's L2 and reused
-// by the row blocks.  Rows >= M and tiles >= Nt load a clamped valid row or
-// tile and are not written.
+// Each XCD (block index mod 8) gets an equal share of the output blocks, a
+// contiguous run in column-block-major order taken in dispatch order: the
+// row blocks of a column block run on one XCD (two where a run boundary
+// splits it), so the block's weights are fetched into that XCD's L2 once and
+// reused, and no XCD gets a second round while others idle.  Rows >= M and
+// tiles >= Nt load a clamped valid row or tile and are not written.
 
 template <bool SYM, int MSW, int NT, int WS>
 __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) k_tiled(TiledArgs a) {
@@ -57,12 +58,15 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const ExtractConsts kx;
-    // block index -> (column block jn, row block im)
+    // block index -> (column block jn, row block im): XCD x (= block index
+    // mod 8) takes an equal contiguous slice of the Gn Mt blocks in
+    // column-block-major order, in dispatch order
     const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3;
-    const int jg = q / a.Mt;                          // once per workgroup
-    const int im = q - jg * a.Mt;
-    const int jn = jg * 8 + xcd;
-    if (jn >= a.Gn) return;                           // uniform: padding of the grid
+    const int nblk = a.Gn * a.Mt, per = nblk >> 3, rem = nblk & 7;
+    if (q >= per + (xcd < rem ? 1 : 0)) return;      // uniform: padding of the grid
+    const int item = xcd * per + min(xcd, rem) + q;
+    const int jn = item / a.Mt;                       // once per workgroup
+    const int im = item - jn * a.Mt;
     const int lm = lane & 15, lg = lane >> 4;
     const DiagSel dsel(lane);
 
@@ -201,6 +205,7 @@ hipError_t launch_tiled_sym(TiledShape sh, const TiledArgs &a, int grid, hipStre
     const dim3 b(kTiledWaves * 64 * tiled_wsplit(sh));
     if (sh.msw == 8 && sh.nt == 4) hipLaunchKernelGGL((k_tiled<SYM, 8, 4, tiled_wsplit({8, 4})>), g, b, 0, st, a);
     else if (sh.msw == 4 && sh.nt == 2) hipLaunchKernelGGL((k_tiled<SYM, 4, 2, tiled_wsplit({4, 2})>), g, b, 0, st, a);
+    else if (sh.msw == 6 && sh.nt == 4) hipLaunchKernelGGL((k_tiled<SYM, 6, 4, tiled_wsplit({6, 4})>), g, b, 0, st, a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
 }

@@ -206,7 +206,8 @@ def test_tiled_matches_oracle(M, K, N):
 @pytest.mark.parametrize("M,K,N,shape", [
     (2100, 256, 16384, "k_tiled<8,4>"),     # 128 x 256 blocks: enough of them for every compute unit
     (1500, 256, 8208, "k_tiled<8,4>"),      # 128 x 256 blocks, partial row and column blocks
-    (1000, 384, 4112, "k_tiled<4,2>"),      # 64 x 128 blocks, partial row and column blocks
+    (1000, 384, 4112, "k_tiled<6,4>"),      # 96 x 256 blocks, partial row and column blocks
+    (1000, 384, 2064, "k_tiled<4,2>"),      # 64 x 128 blocks, partial row and column blocks
     (300, 640, 2576, "k_tiled<4,2>"),       # 64 x 128 blocks for a narrow layer
 ])
 def test_tiled_block_shapes_match_oracle(M, K, N, shape):
