@@ -199,13 +199,20 @@ __device__ inline __amdgpu_buffer_rsrc_t ws_rsrc(const FwdArgs &a) {
 __device__ inline uint32_t ws_region(const FwdArgs &a, int c, int jn) {      // byte offset
     return (uint32_t)((c * a.Gn + jn) * a.TnMax * a.M) * 64u;
 }
-__device__ inline void store_partial8(const FwdArgs &a, const WgWork &w, int it, const float s[8]) {
-    const __amdgpu_buffer_rsrc_t r = ws_rsrc(a);
-    const uint32_t off = ws_region(a, w.c, w.jn) + (uint32_t)it * 32u;
-    __builtin_amdgcn_raw_buffer_store_b128(v4u{__float_as_uint(s[0]), __float_as_uint(s[1]), __float_as_uint(s[2]),
-                                               __float_as_uint(s[3])}, r, off, 0, kSc1);
-    __builtin_amdgcn_raw_buffer_store_b128(v4u{__float_as_uint(s[4]), __float_as_uint(s[5]), __float_as_uint(s[6]),
-                                               __float_as_uint(s[7])}, r, off + 16, 0, kSc1);
+// The four sums of quarter row `it` of the workgroup's output (row m,
+// columns n .. n + 3): bf16 straight to y when the whole K range is covered,
+// else fp32 partials to the workspace, quarter it at float offset 4 it of the
+// region (half row h = (tile * M + m) * 2 + half is quarters 2h and 2h + 1).
+__device__ inline void store_quarter(const FwdArgs &a, const WgWork &w, int it, int m, int n, const float s[4],
+                                     bool direct) {
+    if (direct) {
+        *(uint2 *)(a.y + (size_t)m * a.N + n) = make_uint2(cvt_pk_bf16(s[0], s[1]), cvt_pk_bf16(s[2], s[3]));
+    } else {
+        const uint32_t off = ws_region(a, w.c, w.jn) + (uint32_t)it * 16u;
+        __builtin_amdgcn_raw_buffer_store_b128(
+            v4u{__float_as_uint(s[0]), __float_as_uint(s[1]), __float_as_uint(s[2]), __float_as_uint(s[3])},
+            ws_rsrc(a), off, 0, kSc1);
+    }
 }
 
 // The last of the S workgroups of a column range adds the S fp32 partials in
@@ -229,8 +236,9 @@ __device__ inline void reduce_chunks(const FwdArgs &a, const WgWork &w) {
     __syncthreads();
     if (!s_last) return;
     const __amdgpu_buffer_rsrc_t r = ws_rsrc(a);
-    for (int it = tid; it < items; it += blockDim.x) {
-        const int tl = it / (a.M * 2);
+    const uint32_t inv_pt = 0xFFFFFFFFu / (uint32_t)(a.M * 2) + 1u;   // as in write_out()
+    for (int it = tid; it < items; it += kThreads) {
+        const int tl = (int)__umulhi((uint32_t)it, inv_pt);
         const int rem = it - tl * a.M * 2;
         const int m = rem >> 1, hh = rem & 1;
         const size_t n = (size_t)(w.t0 + tl) * kTileN + 8 * hh;
@@ -270,37 +278,46 @@ __device__ inline void reduce_chunks(const FwdArgs &a, const WgWork &w) {
 // workgroups of this column range adds the S partials in chunk order and
 // writes y.  Every sum runs in a fixed order, so results do not depend on
 // timing: repeated calls give identical bits.
+//
+// The loop strides by the compile-time workgroup size: blockDim.x would be a
+// scalar load of the dispatch's hidden arguments here, after the main loop,
+// and that load misses the scalar cache and costs a memory round trip on the
+// workgroup's critical path.
+//
+// An item's slot reads do not depend on each other: all kWaves of them are
+// issued before the first add (slot wave + tile exists for every wave, so the
+// reads need no guard), and the slots of waves that did not touch the tile
+// are dropped by a select.  Adding 0 for them instead leaves the sum's bits
+// unchanged, so this order equals adding only the touched slots.
 __device__ inline void write_out(const FwdArgs &a, const WgWork &w, const float *slots, int rows) {
     const int tid = threadIdx.x;
-    const int items = w.Tn * a.M * 2;              // half rows of 8 columns
+    const int per_tile = a.M * 4;                  // items (quarter rows of 4 columns) per tile
+    const int items = w.Tn * per_tile;
     const int U = w.Tn * w.Kc;
     const bool direct = (a.S == 1);
-    for (int it = tid; it < items; it += blockDim.x) {
-        const int tl = it / (a.M * 2);
-        const int rem = it - tl * a.M * 2;
-        const int m = rem >> 1, hh = rem & 1;
-        float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    // tile of an item: a multiply-high by ceil(2^32 / per_tile), exact since
+    // items and per_tile stay below 2^16
+    const uint32_t inv_pt = 0xFFFFFFFFu / (uint32_t)per_tile + 1u;
+    for (int it = tid; it < items; it += kThreads) {
+        const int tl = (int)__umulhi((uint32_t)it, inv_pt);
+        const int rem = it - tl * per_tile;
+        const int m = rem >> 2, qq = rem & 3;
+        float4 v[kWaves];
+#pragma unroll
+        for (int i = 0; i < kWaves; ++i)
+            v[i] = *(const float4 *)(slots + ((size_t)(i + tl) * rows + m) * 16 + 4 * qq);
+        float s[4] = {0, 0, 0, 0};
+#pragma unroll
         for (int i = 0; i < kWaves; ++i) {
             int u0, u1;
             wave_range(U, i, u0, u1);
-            if (u0 < u1 && u0 < (tl + 1) * w.Kc && u1 > tl * w.Kc) {
-                const float4 *src = (const float4 *)(slots + ((size_t)(i + tl) * rows + m) * 16 + 8 * hh);
-                const float4 v0 = src[0], v1 = src[1];
-                s[0] += v0.x; s[1] += v0.y; s[2] += v0.z; s[3] += v0.w;
-                s[4] += v1.x; s[5] += v1.y; s[6] += v1.z; s[7] += v1.w;
-            }
+            const bool touched = u0 < u1 && u0 < (tl + 1) * w.Kc && u1 > tl * w.Kc;
+            s[0] += touched ? v[i].x : 0.0f;
+            s[1] += touched ? v[i].y : 0.0f;
+            s[2] += touched ? v[i].z : 0.0f;
+            s[3] += touched ? v[i].w : 0.0f;
         }
-        const size_t n = (size_t)(w.t0 + tl) * kTileN + 8 * hh;
-        if (direct) {
-            uint4 o;
-            o.x = cvt_pk_bf16(s[0], s[1]);
-            o.y = cvt_pk_bf16(s[2], s[3]);
-            o.z = cvt_pk_bf16(s[4], s[5]);
-            o.w = cvt_pk_bf16(s[6], s[7]);
-            *(uint4 *)(a.y + (size_t)m * a.N + n) = o;
-        } else {
-            store_partial8(a, w, it, s);
-        }
+        store_quarter(a, w, it, m, (w.t0 + tl) * kTileN + 4 * qq, s, direct);
     }
     if (!direct) reduce_chunks(a, w);
 }
@@ -368,12 +385,17 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     //    of the device layout, with tl = u / Kc taken as a multiply-high by
     //    ceil(2^32 / Kc) (exact: u and Kc stay below 2^16; Kc = 1, whose
     //    reciprocal needs 33 bits, is taken apart).  All of it is
-    //    wave-uniform scalar arithmetic without branches.  Prefetches past
-    //    the wave's last block re-read that block (a wave with an empty
-    //    range re-reads one block of the workgroup), which is harmless.
+    //    wave-uniform scalar arithmetic without branches.
     //    The loads go through buffer resources based at the workgroup's first
     //    block (its blocks span at most Tn Kb KiB, well inside the 32-bit
     //    range), so the block offset is a scalar operand of the load.
+    //    Prefetches past the wave's last block (the last kDepth of the loop,
+    //    or all of them for a wave with an empty range) are never consumed:
+    //    they go through a resource of size zero, so every path still issues
+    //    the same loads (the wait counts stay static) but these return zero
+    //    without touching memory.  Re-reading a real block instead would keep
+    //    the wave waiting a full memory round trip after its last block,
+    //    since the code after the loop reuses their registers.
     const bool kc1 = w.Kc == 1;
     const uint32_t inv_kc = kc1 ? 0u : 0xFFFFFFFFu / (uint32_t)w.Kc + 1u;
     const uint32_t kc1_mask = kc1 ? 0xFFFFFFFFu : 0u;       // selects u itself when Kc == 1, without a branch
@@ -487,30 +509,27 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
 template <int TN>
 __device__ inline void write_out_waves(const FwdArgs &a, const WgWork &w, const float *slots, int rows) {
     const int tid = threadIdx.x;
-    const int items = w.Tn * a.M * 2;              // half rows of 8 columns
+    const int per_tile = a.M * 4;                  // items (quarter rows of 4 columns) per tile
+    const int items = w.Tn * per_tile;
     const bool direct = (a.S == 1);
-    for (int it = tid; it < items; it += blockDim.x) {
-        const int tl = it / (a.M * 2);
-        const int rem = it - tl * a.M * 2;
-        const int m = rem >> 1, hh = rem & 1;
-        float s[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    const uint32_t inv_pt = 0xFFFFFFFFu / (uint32_t)per_tile + 1u;   // as in write_out()
+    for (int it = tid; it < items; it += kThreads) {
+        const int tl = (int)__umulhi((uint32_t)it, inv_pt);
+        const int rem = it - tl * per_tile;
+        const int m = rem >> 2, qq = rem & 3;
+        float4 v[kWaves];
+#pragma unroll
+        for (int i = 0; i < kWaves; ++i)
+            v[i] = *(const float4 *)(slots + (((size_t)i * TN + tl) * rows + m) * 16 + 4 * qq);
+        float s[4] = {0, 0, 0, 0};
+#pragma unroll
         for (int i = 0; i < kWaves; ++i) {
-            const float4 *src = (const float4 *)(slots + (((size_t)i * TN + tl) * rows + m) * 16 + 8 * hh);
-            const float4 v0 = src[0], v1 = src[1];
-            s[0] += v0.x; s[1] += v0.y; s[2] += v0.z; s[3] += v0.w;
-            s[4] += v1.x; s[5] += v1.y; s[6] += v1.z; s[7] += v1.w;
+            s[0] += v[i].x;
+            s[1] += v[i].y;
+            s[2] += v[i].z;
+            s[3] += v[i].w;
         }
-        const size_t n = (size_t)(w.t0 + tl) * kTileN + 8 * hh;
-        if (direct) {
-            uint4 o;
-            o.x = cvt_pk_bf16(s[0], s[1]);
-            o.y = cvt_pk_bf16(s[2], s[3]);
-            o.z = cvt_pk_bf16(s[4], s[5]);
-            o.w = cvt_pk_bf16(s[6], s[7]);
-            *(uint4 *)(a.y + (size_t)m * a.N + n) = o;
-        } else {
-            store_partial8(a, w, it, s);
-        }
+        store_quarter(a, w, it, m, (w.t0 + tl) * kTileN + 4 * qq, s, direct);
     }
     if (!direct) reduce_chunks(a, w);
 }
