@@ -272,8 +272,9 @@ __device__ inline void reduce_chunks(const FwdArgs &a, const WgWork &w) {
 }
 
 // Writes the workgroup's results.  Each wave left one partial sum per column
-// tile it touched in LDS slot (wave + tile); the tile's sum adds those slots in
-// wave order.  With the whole K range covered (S == 1) the sum goes to y as
+// tile it touched in LDS slot (wave, tile), and zeros (from the kernel's start)
+// in the slots of the tiles it did not touch; the tile's sum adds the slots of
+// all waves in wave order.  With the whole K range covered (S == 1) the sum goes to y as
 // bf16; otherwise it goes to the fp32 workspace, and the last of the S
 // workgroups of this column range adds the S partials in chunk order and
 // writes y.  Every sum runs in a fixed order, so results do not depend on
@@ -285,15 +286,13 @@ __device__ inline void reduce_chunks(const FwdArgs &a, const WgWork &w) {
 // workgroup's critical path.
 //
 // An item's slot reads do not depend on each other: all kWaves of them are
-// issued before the first add (slot wave + tile exists for every wave, so the
-// reads need no guard), and the slots of waves that did not touch the tile
-// are dropped by a select.  Adding 0 for them instead leaves the sum's bits
-// unchanged, so this order equals adding only the touched slots.
+// issued before the first add.  Adding the zero slots leaves a sum's bits
+// unchanged (the sum starts at +0), so the result equals the sum of the
+// touched slots alone, without a per-slot test.
 __device__ inline void write_out(const FwdArgs &a, const WgWork &w, const float *slots, int rows) {
     const int tid = threadIdx.x;
     const int per_tile = a.M * 4;                  // items (quarter rows of 4 columns) per tile
     const int items = w.Tn * per_tile;
-    const int U = w.Tn * w.Kc;
     const bool direct = (a.S == 1);
     // tile of an item: a multiply-high by ceil(2^32 / per_tile), exact since
     // items and per_tile stay below 2^16
@@ -305,17 +304,14 @@ __device__ inline void write_out(const FwdArgs &a, const WgWork &w, const float 
         float4 v[kWaves];
 #pragma unroll
         for (int i = 0; i < kWaves; ++i)
-            v[i] = *(const float4 *)(slots + ((size_t)(i + tl) * rows + m) * 16 + 4 * qq);
+            v[i] = *(const float4 *)(slots + ((size_t)(i * w.Tn + tl) * rows + m) * 16 + 4 * qq);
         float s[4] = {0, 0, 0, 0};
 #pragma unroll
         for (int i = 0; i < kWaves; ++i) {
-            int u0, u1;
-            wave_range(U, i, u0, u1);
-            const bool touched = u0 < u1 && u0 < (tl + 1) * w.Kc && u1 > tl * w.Kc;
-            s[0] += touched ? v[i].x : 0.0f;
-            s[1] += touched ? v[i].y : 0.0f;
-            s[2] += touched ? v[i].z : 0.0f;
-            s[3] += touched ? v[i].w : 0.0f;
+            s[0] += v[i].x;
+            s[1] += v[i].y;
+            s[2] += v[i].z;
+            s[3] += v[i].w;
         }
         store_quarter(a, w, it, m, (w.t0 + tl) * kTileN + 4 * qq, s, direct);
     }
@@ -330,7 +326,8 @@ __device__ inline void write_out(const FwdArgs &a, const WgWork &w, const float 
 // LDS write instructions) while its first weight blocks are already in
 // flight; its waves then split the Tn * Kc blocks evenly (tile-major order),
 // each keeping kDepth 1 KiB blocks in flight.  A wave leaves one partial sum
-// per tile it touches in an LDS slot; write_out() adds them in a fixed order.
+// per tile it touches in its LDS slot for that tile (slots start at zero);
+// write_out() adds the waves' slots in a fixed order.
 //
 // x in LDS: 16-byte fragments, fragment (row, q8) = x[row][k0 .. k0 + 8)
 // with k0 = 128 g0 + 8 q8 (q8 = 16 kbl + c, c = 4j + g < 16), row-major at
@@ -355,7 +352,7 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     const int n8 = w.Kc * 16;                         // 16-byte chunks per row of the x chunk
     const int nslots = XR * (n8 + 1);
     const int nload = (nslots + 63) >> 6;             // direct-to-LDS loads of the workgroup
-    float *slots = (float *)(smem + (size_t)nload * 1024);
+    float *slots = (float *)(smem + (size_t)nload * 1024);   // [kWaves][Tn][MR][16] partial sums
 
     const int U = w.Tn * w.Kc;
     int u0, u1;
@@ -424,6 +421,12 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     };
 #pragma unroll
     for (int d = 0; d < kDepth; ++d) fetch(d, (uint32_t)(u0 + d));
+    // the partial-sum slots start at zero (a wave writes only the slots of
+    // the tiles it touches); the barrier below orders this before any write
+    {
+        const int nq = kWaves * w.Tn * MR * 4;     // 16-byte words
+        for (int i = tid; i < nq; i += kThreads) ((float4 *)slots)[i] = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    }
     // 3) every wave's x loads have landed in LDS (only the weight prefetch,
     //    2 kDepth loads, may still be in flight)
     asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * kDepth) : "memory");
@@ -465,7 +468,7 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
                 // D of the 16x16 op: lane l holds rows n = 4(l >> 4) + v of column m = l & 15
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt) {
-                    *(v4f *)(slots + ((size_t)(wave + tl) * MR + 16 * mt + lm) * 16 + 4 * lg) = acc[mt];
+                    *(v4f *)(slots + ((size_t)(wave * w.Tn + tl) * MR + 16 * mt + lm) * 16 + 4 * lg) = acc[mt];
                     acc[mt] = v4f{0, 0, 0, 0};
                 }
             }

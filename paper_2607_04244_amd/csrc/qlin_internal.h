@@ -95,12 +95,11 @@ inline size_t lds_bytes_regs(int rows, int tn) { return (size_t)kWaves * tn * ro
 // (staged_rows(M) rows of 16 Kc + 1 slots of 16 bytes, in whole 1 KiB
 // direct-to-LDS loads) plus one
 // partial-sum slot (16 m-columns per m-tile x 16 fp32) per (wave, column
-// tile) pair a wave touches; slot = wave + tile is unique, so kWaves + Tn - 1
-// slots suffice.
+// tile) pair.
 inline size_t lds_bytes(int M, int Kc, int Tn) {
     const int mrows = 16 * ((M + 15) / 16);
     const size_t x = ((size_t)staged_rows(M) * (Kc * 16 + 1) * 16 + 1023) / 1024 * 1024;
-    return x + (size_t)(kWaves + Tn) * mrows * 16 * 4;
+    return x + (size_t)kWaves * Tn * mrows * 16 * 4;
 }
 
 // Host launchers (kernels.hip).  Each returns the launch status.
