@@ -293,8 +293,8 @@ constexpr TunedPlan kTunedPlans[] = {
     {13, 16, 2560, 4096, kKernStaged, 1},   // q projection
     {14, 16, 4096, 2560, kKernStaged, 1},   // o projection
     {1, 4, 9728, 2560, kKernStaged, 1},     // down projection
-    {12, 15, 9728, 2560, kKernMfma16, 3},
-    {16, 16, 9728, 2560, kKernMfma16, 5},
+    {8, 15, 9728, 2560, kKernMfma16, 3},
+    {16, 16, 9728, 2560, kKernStaged, 3},
 };
 
 const TunedPlan *tuned_plan(const qlin_s *h, int M) {
@@ -385,11 +385,14 @@ int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
         if ((int64_t)Tn * h->Kb * 1024 >= ((int64_t)1 << 31)) return false;   // span of its buffer descriptors
         return lds_bytes(Mi, Kc, Tn) <= kLdsMax;
     };
-    // column ranges for S chunks: about one workgroup per CU, but no range
-    // wider than the kernel's tile limit (and more ranges if LDS demands)
+    // column ranges for S chunks: one workgroup per CU (never more: a second
+    // round of workgroups would double the time), but no range wider than the
+    // kernel's tile limit (and more ranges if LDS demands).  Uneven ranges are
+    // fine: splitting the columns over fewer, equal ranges leaves CUs idle,
+    // and was measured slower.
     auto gn_for = [&](int kern, int S) {
         const int tm = tn_max_of(kern);
-        int Gn = std::max((h->Nt + tm - 1) / tm, std::min(h->Nt, (int)std::lround((double)h->num_cu / S)));
+        int Gn = std::max((h->Nt + tm - 1) / tm, std::min(h->Nt, std::max(1, h->num_cu / S)));
         Gn = std::min(Gn, h->Nt);
         while (Gn < h->Nt && !fits(kern, S, Gn)) ++Gn;
         return Gn;

@@ -356,7 +356,8 @@ def test_forward_argument_errors():
     (16, 2560, 19456, "k_skinny<1,16>", 1),    # the draft-block verification linear
     (16, 2560, 6144, "k_skinny<1,16>", 1),     # q|k|v of a layer
     (16, 4096, 2560, "k_skinny<1,16>", 1),     # o projection (measured plan)
-    (16, 9728, 2560, "k_mfma16<4>", 5),        # down projection (measured plan)
+    (16, 9728, 2560, "k_skinny<1,16>", 3),     # down projection (measured plan)
+    (8, 9728, 2560, "k_mfma16<2>", 3),         # down projection, half a draft block (measured plan)
     (1, 9728, 2560, "k_skinny<1,1>", 1),       # down projection, one row (measured plan)
     (1, 2560, 2560, "k_mfma16<1>", 1),         # single-row layer
 ])
