@@ -28,6 +28,14 @@ __host__ __device__ inline void block_coord(int l, int j, int p, int &n16, int &
     k128 = 32 * j + 8 * (l >> 4) + 4 * h + (l & 3);
 }
 
+// Buffer-resource constants.  Cross-workgroup partial sums travel between
+// workgroups that may sit on different XCDs, whose L2 caches are not coherent
+// with each other for ordinary accesses: they are written and read with
+// agent-scope (sc1) buffer accesses, which the hardware performs at the
+// device coherence point.
+constexpr int kSc1 = 16;                 // cache-policy operand of the buffer builtins: sc1 (agent scope)
+constexpr int kRsrcFlags = 0x00020000;   // buffer descriptor word 3: 32-bit raw data
+
 // ------------------------------------------------------------------ small helpers
 
 __device__ inline uint32_t cvt_pk_bf16(float lo, float hi) {

@@ -190,8 +190,6 @@ __device__ inline void wave_range(int U, int i, int &u0, int &u1) {
 // contiguous region of TnMax * M * 16 fp32 at ((c * Gn + jn) * TnMax * M * 16),
 // item it = (tile * M + m) * 2 + half at float offset 8 * it, so the 16-byte
 // accesses of a wave are contiguous.
-constexpr int kSc1 = 16;   // cache-policy operand of the buffer builtins: sc1 (agent scope)
-constexpr int kRsrcFlags = 0x00020000;   // buffer descriptor word 3: 32-bit raw data
 
 __device__ inline __amdgpu_buffer_rsrc_t ws_rsrc(const FwdArgs &a) {
     return __builtin_amdgcn_make_buffer_rsrc(a.ws, 0, (int)a.ws_bytes, kRsrcFlags);

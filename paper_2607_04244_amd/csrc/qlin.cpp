@@ -28,7 +28,8 @@ struct qlin_s {
     void *sz = nullptr;          // Nt * Kb * 16 entries (u32 s|z<<16, or u16 s)
     float *ws = nullptr;         // split-K partials, ws_floats fp32
     int ws_rows = 0;             // S * M the workspace covers for any column split
-    size_t ws_floats = 0;        // 2 * ws_rows * N >= S * Gn * TnMax * M * 16 when S * M <= ws_rows
+    size_t ws_floats = 0;        // allocated fp32 (also covers one 64 x 128 partial block per CU)
+    size_t ws_decode = 0;        // 2 * ws_rows * N >= S * Gn * TnMax * M * 16 when S * M <= ws_rows
     uint32_t *counters = nullptr;
     int counters_n = 0;
 };
@@ -183,7 +184,6 @@ qlin_t create_impl(int64_t K, int64_t N, int64_t group, const uint32_t *packed, 
     h->symmetric = symmetric;
     const size_t code_bytes = (size_t)N * K / 2;
     const size_t sz_bytes = ngroups * (symmetric ? 2 : 4);
-    h->counters_n = std::max(h->Nt, 1);
     // rows of partial sums the smallest feasible K split needs, for every M
     // a SKINNY launch can have (the other kernels need no split)
     h->ws_rows = kWsRowsMin;
@@ -205,17 +205,22 @@ qlin_t create_impl(int64_t K, int64_t N, int64_t group, const uint32_t *packed, 
     };
     if ((e = dev_alloc((void **)&h->codes, code_bytes)) != hipSuccess) return bail("codes", e);
     if ((e = dev_alloc(&h->sz, sz_bytes)) != hipSuccess) return bail("scales", e);
-    h->ws_floats = 2 * (size_t)h->ws_rows * N;
-    if (h->ws_floats * 4 > 0xFFFFFFF0u) h->ws_floats = 0xFFFFFFF0u / 4;   // buffer descriptor range
+    if ((e = hipGetDevice(&h->device)) != hipSuccess) return bail("hipGetDevice", e);
+    if ((e = hipDeviceGetAttribute(&h->num_cu, hipDeviceAttributeMultiprocessorCount, h->device)) != hipSuccess)
+        return bail("hipDeviceGetAttribute", e);
+    // arrival counters: one per column range of the decode kernels, or per
+    // output block of a K-split tiled launch (at most one per CU)
+    h->counters_n = std::max(h->Nt, h->num_cu);
+    // partial sums: the decode kernels' smallest feasible split for every M,
+    // and one 64 x 128 fp32 partial block per CU for a K-split tiled launch
+    h->ws_decode = std::min(2 * (size_t)h->ws_rows * N, (size_t)0xFFFFFFF0u / 4);   // buffer descriptor range
+    h->ws_floats = std::max(h->ws_decode, std::min((size_t)h->num_cu * 64 * 128, (size_t)0xFFFFFFF0u / 4));
     if ((e = dev_alloc((void **)&h->ws, h->ws_floats * 4)) != hipSuccess) return bail("workspace", e);
     if ((e = dev_alloc((void **)&h->counters, (size_t)h->counters_n * 4)) != hipSuccess) return bail("counters", e);
     if ((e = dev_alloc(&canon, code_bytes)) != hipSuccess) return bail("staging", e);
     if ((e = dev_alloc(&sc, ngroups * 2)) != hipSuccess) return bail("staging", e);
     if (!symmetric && (e = dev_alloc(&zc, ngroups * 2)) != hipSuccess) return bail("staging", e);
 
-    if ((e = hipGetDevice(&h->device)) != hipSuccess) return bail("hipGetDevice", e);
-    if ((e = hipDeviceGetAttribute(&h->num_cu, hipDeviceAttributeMultiprocessorCount, h->device)) != hipSuccess)
-        return bail("hipDeviceGetAttribute", e);
     static std::once_flag once;
     std::call_once(once, [] { (void)prepare_kernels(); (void)hipGetLastError(); });
     if ((e = hipMemcpy(canon, packed, code_bytes, hipMemcpyDefault)) != hipSuccess)
@@ -312,45 +317,83 @@ const TunedPlan *tuned_plan(const qlin_s *h, int M) {
 // within 2%): small blocks for narrow layers at small M, 96 x 256 where 128
 // rows would leave part of the chip idle, 128 x 256 otherwise.
 int make_tiled_plan(const qlin_s *h, int64_t split_k, int64_t M, Plan *p) {
-    if (split_k > 1) return fail(QLIN_ERR_UNSUPPORTED, "split_k=%d does not fit (TILED path runs the whole K range)", (int)split_k);
+    if (split_k < 0 || split_k > h->Kb) return fail(QLIN_ERR_INVALID, "split_k must be in [0, K/128]");
     if (M * h->K >= ((int64_t)1 << 31)) return fail(QLIN_ERR_UNSUPPORTED, "TILED path needs M * K < 2^31");
-    constexpr double kBlockTime[] = {1.0, 0.42, 0.95};           // per kTiledShapes entry
-    static_assert(sizeof kBlockTime / sizeof kBlockTime[0] == sizeof kTiledShapes / sizeof kTiledShapes[0], "");
-    TiledShape sh = kTiledShapes[0];
-    double best = 1e300;
-    for (int i = 0; i < (int)(sizeof kTiledShapes / sizeof kTiledShapes[0]); ++i) {
-        const TiledShape c = kTiledShapes[i];
-        const int64_t blocks = ((M + 16 * c.msw - 1) / (16 * c.msw)) * ((h->Nt + 4 * c.nt - 1) / (4 * c.nt));
-        const double t = (double)((blocks + h->num_cu - 1) / h->num_cu) * kBlockTime[i];
-        if (t < best) { best = t; sh = c; }
-    }
+    constexpr int kShapes = (int)(sizeof kTiledShapes / sizeof kTiledShapes[0]);
     static const int forced = [] {                   // tuning knob: QLIN_TILED_SHAPE = index into kTiledShapes
         const char *e = getenv("QLIN_TILED_SHAPE");
         return e ? atoi(e) : -1;
     }();
-    if (forced >= 0 && forced < (int)(sizeof kTiledShapes / sizeof kTiledShapes[0])) sh = kTiledShapes[forced];
+    auto allowed = [&](int i) { return forced < 0 || forced >= kShapes || i == forced; };
+    auto blocks_of = [&](int i) {
+        const TiledShape c = kTiledShapes[i];
+        return ((M + 16 * c.msw - 1) / (16 * c.msw)) * (int64_t)((h->Nt + 4 * c.nt - 1) / (4 * c.nt));
+    };
+    // Whole K range: the shape that minimises (blocks per compute unit,
+    // rounded up) x (block time relative to 128 x 256).
+    constexpr double kBlockTime[] = {1.0, 0.42, 0.95};
+    static_assert(sizeof kBlockTime / sizeof kBlockTime[0] == kShapes, "");
+    int best_i = -1, best_s = 1;
+    double best = 1e300;
+    for (int i = 0; i < kShapes; ++i) {
+        if (!allowed(i)) continue;
+        const double t = (double)((blocks_of(i) + h->num_cu - 1) / h->num_cu) * kBlockTime[i];
+        if (t < best) { best = t; best_i = i; }
+    }
+    // A K split, when that leaves more than half the CUs idle (or when one is
+    // asked for).  Time model in us: a pipeline ramp plus a time per 128-wide
+    // group of K per block with every CU busy (128 x 256: 2.28, 64 x 128: 0.97,
+    // 96 x 256: 2.17), times the rounds of work items over the CUs; a split
+    // adds the exchange: ~3 us of latency plus the partial blocks written and
+    // read back at ~4 TB/s.
+    if (split_k > 1 || (split_k == 0 && blocks_of(best_i) * 2 <= h->num_cu)) {
+        constexpr double kRamp = 2.0, kGroupTime[] = {2.28, 0.97, 2.17}, kExchange = 3.0, kPartialBw = 4.0e6;
+        static_assert(sizeof kGroupTime / sizeof kGroupTime[0] == kShapes, "");
+        best_i = -1;
+        best = 1e300;
+        for (int i = 0; i < kShapes; ++i) {
+            if (!allowed(i)) continue;
+            const TiledShape c = kTiledShapes[i];
+            const double bm = 16.0 * c.msw, bn = 64.0 * c.nt;
+            const int64_t blocks = blocks_of(i);
+            const int s_lo = split_k > 0 ? (int)split_k : 1;
+            const int s_hi = split_k > 0 ? (int)split_k : std::min(16, h->Kb);
+            for (int S = s_lo; S <= s_hi; ++S) {
+                if (S > 1) {   // partial blocks and arrival counters must fit the handle's buffers
+                    if (blocks > h->counters_n) continue;
+                    if ((double)S * blocks * bm * bn > (double)h->ws_floats) continue;
+                }
+                const int Kc = (h->Kb + S - 1) / S;
+                const double rounds = (double)((blocks * S + h->num_cu - 1) / h->num_cu);
+                double t = rounds * (kRamp + kGroupTime[i] * Kc);
+                if (S > 1) t += kExchange + 2.0 * S * blocks * bm * bn * 4.0 / kPartialBw;
+                if (t < best) { best = t; best_i = i; best_s = S; }
+            }
+        }
+    }
+    if (best_i < 0) return fail(QLIN_ERR_UNSUPPORTED, "split_k=%d does not fit (workspace or counters)", (int)split_k);
+    const TiledShape sh = kTiledShapes[best_i];
     const int Mt = (int)((M + 16 * sh.msw - 1) / (16 * sh.msw));
     const int Gn = (h->Nt + 4 * sh.nt - 1) / (4 * sh.nt);
     p->path = kTiled;
     p->kern = kKernTiled;
     p->mrows = 16 * sh.msw;
-    p->S = 1;
+    p->S = best_s;
     p->Gn = Gn;
     p->tn = sh.nt;
-    p->grid = 8 * ((Gn * Mt + 7) / 8);
+    p->grid = 8 * ((Gn * Mt * best_s + 7) / 8);
     p->lds = 0;
     return QLIN_OK;
 }
 
 // Does the automatic choice run M rows through the TILED kernel (one
-// launch) rather than 64-row slices of the decode kernels?  Measured on
-// MI355X: from M = 256 on the tiled kernel always wins; at M = 128 it wins
-// once it has about 64 blocks of 64 x 128 (q|k|v, gate|up), and the narrow
-// layers (o, down: 40 blocks) are faster as two slices.
+// launch) rather than 64-row slices of the decode kernels?  Above 64 rows,
+// always: with its K split the tiled kernel also covers the narrow, deep
+// layers at small M (measured on MI355X at M = 128: o projection 14.5 us
+// against 35.9 us as two slices, down projection 21.8 us against 74.2 us).
 bool auto_tiled(const qlin_s *h, int64_t M) {
-    if (M <= kMaxSkinnyM) return false;
-    const int64_t blocks = ((M + 63) / 64) * ((h->Nt + 7) / 8);      // 64 x 128 blocks
-    return M >= 256 || blocks >= 64;
+    (void)h;
+    return M > kMaxSkinnyM;
 }
 
 int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
@@ -377,7 +420,7 @@ int make_plan(const qlin_s *h, int path, int64_t split_k, int64_t M, Plan *p) {
     auto rows_of = [&](int kern) { return kern == kKernGemv ? Mi : 16 * ((Mi + 15) / 16); };
     auto fits = [&](int kern, int S, int Gn) {
         const int Kc = (h->Kb + S - 1) / S, Tn = (h->Nt + Gn - 1) / Gn;
-        if (S > 1 && (size_t)S * Gn * Tn * Mi * 16 > h->ws_floats) return false;
+        if (S > 1 && (size_t)S * Gn * Tn * Mi * 16 > h->ws_decode) return false;
         if (Gn > h->counters_n || Tn > tn_max_of(kern)) return false;
         if (kern != kKernStaged) return lds_bytes_regs(rows_of(kern), Tn) <= kLdsMax;
         if (!chunk_fits(Mi, Kc)) return false;
@@ -480,6 +523,12 @@ int run_forward(qlin_s *h, int path, int64_t split_k, int64_t M, const uint16_t 
         a.Nt = h->Nt;
         a.Mt = (int)((M + p.mrows - 1) / p.mrows);
         a.Gn = p.Gn;
+        a.S = p.S;
+        a.Kq = h->Kb / p.S;
+        a.Kr = h->Kb % p.S;
+        a.ws = h->ws;
+        a.counters = h->counters;
+        a.ws_bytes = (uint32_t)(h->ws_floats * 4);
         e = launch_tiled(h->symmetric, TiledShape{p.mrows / 16, p.tn}, a, p.grid, st);
         if (e != hipSuccess) return hip_fail(e, "tiled launch");
         return QLIN_OK;

@@ -76,6 +76,11 @@ struct TiledArgs {
     int M, K, N, Kb, Nt;
     int Mt;                 // row blocks: ceil(M / (16 MSW))
     int Gn;                 // column blocks: ceil(Nt / (4 NT))
+    int S;                  // K chunks; chunk c holds Kq (+1 for c < Kr) groups
+    int Kq, Kr;
+    float *ws;              // S > 1: fp32 partial blocks, Gn Mt S of 16 MSW x 64 NT
+    uint32_t *counters;     // S > 1: [Gn Mt] arrival counters, zero between launches
+    uint32_t ws_bytes;      // size of ws
 };
 
 // Rows of x a SKINNY workgroup keeps in LDS for M rows (M <= 64): the next

@@ -33,14 +33,24 @@ namespace qlin {
 // the global reads stay coalesced), and the operand reads (16 lanes = 16
 // rows of one c) hit 16 distinct bank groups.
 //
-// Each XCD (block index mod 8) gets an equal share of the output blocks, a
+// Each XCD (block index mod 8) gets an equal share of the work items, a
 // contiguous run in column-block-major order taken in dispatch order: the
 // row blocks of a column block run on one XCD (two where a run boundary
 // splits it), so the block's weights are fetched into that XCD's L2 once and
 // reused, and no XCD gets a second round while others idle.  Rows >= M and
 // tiles >= Nt load a clamped valid row or tile and are not written.
+//
+// With few output blocks (small M over a narrow layer) the K range is cut in
+// S chunks: work item (block, chunk c) covers groups [g0, g0 + Kc) of its
+// block and stores its fp32 partial block with agent-scope stores; the last
+// of the S workgroups of a block to arrive (one relaxed atomic per workgroup,
+// after its stores have completed) reads the S partials back and adds them
+// in chunk order (a fixed order: repeated calls give identical bits), and
+// writes y.  Partial block (block, c) sits at float
+// offset (block S + c) BM BN, element (ms, tile, lane) at 4 ((ms 4 NT + tile)
+// 64 + lane): one 16-byte access per lane and product.
 
-template <bool SYM, int MSW, int NT, int WS>
+template <bool SYM, int MSW, int NT, int WS, bool SPLIT>
 __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) k_tiled(TiledArgs a) {
     constexpr int kWavesWg = kTiledWaves * WS;
     constexpr int BM = 16 * MSW;
@@ -58,15 +68,19 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const ExtractConsts kx;
-    // block index -> (column block jn, row block im): XCD x (= block index
-    // mod 8) takes an equal contiguous slice of the Gn Mt blocks in
-    // column-block-major order, in dispatch order
+    // block index -> (column block jn, row block im, K chunk c): XCD x (=
+    // block index mod 8) takes an equal contiguous slice of the Gn Mt S work
+    // items in column-block-major order, in dispatch order
     const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3;
-    const int nblk = a.Gn * a.Mt, per = nblk >> 3, rem = nblk & 7;
+    const int nitem = a.Gn * a.Mt * (SPLIT ? a.S : 1), per = nitem >> 3, rem = nitem & 7;
     if (q >= per + (xcd < rem ? 1 : 0)) return;      // uniform: padding of the grid
     const int item = xcd * per + min(xcd, rem) + q;
-    const int jn = item / a.Mt;                       // once per workgroup
-    const int im = item - jn * a.Mt;
+    const int blk = SPLIT ? item / a.S : item;        // once per workgroup
+    const int c = SPLIT ? item - blk * a.S : 0;
+    const int jn = blk / a.Mt;
+    const int im = blk - jn * a.Mt;
+    const int g0 = SPLIT ? c * a.Kq + min(c, a.Kr) : 0;   // the chunk's groups [g0, g1]
+    const int g1 = SPLIT ? g0 + a.Kq + (c < a.Kr ? 1 : 0) - 1 : a.Kb - 1;
     const int lm = lane & 15, lg = lane >> 4;
     const DiagSel dsel(lane);
 
@@ -167,14 +181,14 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     constexpr int S = kTiledStages;
 #pragma unroll
     for (int i = 0; i < S - 1; ++i) {
-        load_x(min(i, a.Kb - 1), i);
-        load_w(min(i, a.Kb - 1), i);
+        load_x(min(g0 + i, g1), i);
+        load_w(min(g0 + i, g1), i);
     }
     int buf = 0;
-    for (int kb = 0; kb < a.Kb; ++kb) {
-        const int nb = buf == 0 ? S - 1 : buf - 1;             // (kb + S - 1) % S
-        load_x(min(kb + S - 1, a.Kb - 1), nb);
-        load_w(min(kb + S - 1, a.Kb - 1), nb);
+    for (int kb = g0; kb <= g1; ++kb) {
+        const int nb = buf == 0 ? S - 1 : buf - 1;             // (kb - g0 + S - 1) % S
+        load_x(min(kb + S - 1, g1), nb);
+        load_w(min(kb + S - 1, g1), nb);
         asm volatile("s_waitcnt vmcnt(%0)" :: "n"((S - 1) * kIssued) : "memory");
         lds_barrier();                        // group kb is in LDS for every wave
         compute(buf);
@@ -182,6 +196,66 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
         buf = buf == S - 1 ? 0 : buf + 1;
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the reloads past the end
+
+    if constexpr (SPLIT) {
+        // partial block to the workspace, then the arrival count; the last
+        // arrival of the block sums the S partials in chunk order
+        constexpr int kBlkFloats = BM * 64 * NT;
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(a.ws, 0, (int)a.ws_bytes, kRsrcFlags);
+        auto part_off = [&](int cc, int ms, int t) {   // byte offset of this lane's 16 bytes
+            return (uint32_t)(((size_t)blk * a.S + cc) * kBlkFloats * 4) +
+                   (uint32_t)(((ms * kTiles + wave * NW + t) * 64 + lane) * 16);
+        };
+#pragma unroll
+        for (int ms = 0; ms < MSW; ++ms)
+#pragma unroll
+            for (int t = 0; t < NW; ++t)
+                __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(v4u, acc[ms][t]), r, part_off(c, ms, t), 0,
+                                                       kSc1);
+        __shared__ int s_last;
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        if (tid == 0) {
+            const uint32_t old = __hip_atomic_fetch_add(&a.counters[blk], 1u, __ATOMIC_RELAXED,
+                                                        __HIP_MEMORY_SCOPE_AGENT);
+            s_last = (old == (uint32_t)(a.S - 1));
+        }
+        __syncthreads();
+        if (!s_last) return;
+        // kBatch chunks of all the lane's MSW NW products are loaded together
+        // (one memory round trip per batch), then added in chunk order
+        constexpr int kBatch = MSW * NW >= 32 ? 1 : 32 / (MSW * NW);
+        v4f sum[MSW][NW];
+#pragma unroll
+        for (int ms = 0; ms < MSW; ++ms)
+#pragma unroll
+            for (int t = 0; t < NW; ++t) sum[ms][t] = v4f{0, 0, 0, 0};
+        for (int c0 = 0; c0 < a.S; c0 += kBatch) {
+            v4f v[kBatch][MSW][NW];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int cc = min(c0 + u, a.S - 1);      // unconditional load; extra ones are not added
+#pragma unroll
+                for (int ms = 0; ms < MSW; ++ms)
+#pragma unroll
+                    for (int t = 0; t < NW; ++t)
+                        v[u][ms][t] = __builtin_bit_cast(
+                            v4f, __builtin_amdgcn_raw_buffer_load_b128(r, part_off(cc, ms, t), 0, kSc1));
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u)
+                if (c0 + u < a.S)
+#pragma unroll
+                    for (int ms = 0; ms < MSW; ++ms)
+#pragma unroll
+                        for (int t = 0; t < NW; ++t) sum[ms][t] += v[u][ms][t];
+        }
+#pragma unroll
+        for (int ms = 0; ms < MSW; ++ms)
+#pragma unroll
+            for (int t = 0; t < NW; ++t) acc[ms][t] = sum[ms][t];
+        if (tid == 0) __hip_atomic_store(&a.counters[blk], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
 
     // D of the 16x16 op: lane l holds rows n = 4 (l >> 4) + v of column m = l & 15
 #pragma unroll
@@ -199,15 +273,22 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     }
 }
 
-template <bool SYM>
-hipError_t launch_tiled_sym(TiledShape sh, const TiledArgs &a, int grid, hipStream_t st) {
+template <bool SYM, bool SPLIT>
+hipError_t launch_tiled_kernel(TiledShape sh, const TiledArgs &a, int grid, hipStream_t st) {
     const dim3 g(grid);
     const dim3 b(kTiledWaves * 64 * tiled_wsplit(sh));
-    if (sh.msw == 8 && sh.nt == 4) hipLaunchKernelGGL((k_tiled<SYM, 8, 4, tiled_wsplit({8, 4})>), g, b, 0, st, a);
-    else if (sh.msw == 4 && sh.nt == 2) hipLaunchKernelGGL((k_tiled<SYM, 4, 2, tiled_wsplit({4, 2})>), g, b, 0, st, a);
-    else if (sh.msw == 6 && sh.nt == 4) hipLaunchKernelGGL((k_tiled<SYM, 6, 4, tiled_wsplit({6, 4})>), g, b, 0, st, a);
+    if (sh.msw == 8 && sh.nt == 4) hipLaunchKernelGGL((k_tiled<SYM, 8, 4, tiled_wsplit({8, 4}), SPLIT>), g, b, 0, st, a);
+    else if (sh.msw == 4 && sh.nt == 2) hipLaunchKernelGGL((k_tiled<SYM, 4, 2, tiled_wsplit({4, 2}), SPLIT>), g, b, 0, st, a);
+    else if (sh.msw == 6 && sh.nt == 4) hipLaunchKernelGGL((k_tiled<SYM, 6, 4, tiled_wsplit({6, 4}), SPLIT>), g, b, 0, st, a);
     else return hipErrorInvalidValue;
     return hipGetLastError();
+}
+
+// The whole-K kernel is a separate instantiation from the K-split one, so
+// that the split's epilogue does not weigh on its register allocation.
+template <bool SYM>
+hipError_t launch_tiled_sym(TiledShape sh, const TiledArgs &a, int grid, hipStream_t st) {
+    return a.S > 1 ? launch_tiled_kernel<SYM, true>(sh, a, grid, st) : launch_tiled_kernel<SYM, false>(sh, a, grid, st);
 }
 
 hipError_t launch_tiled(bool symmetric, TiledShape shape, const TiledArgs &a, int grid, hipStream_t st) {
