@@ -78,6 +78,16 @@ __device__ inline Pairs extract_pairs(uint32_t P, const ExtractConsts &k) {
 // One lane's 16 bytes of a weight block.
 __device__ inline uint4 load_block(const uint4 *codes, size_t idx) { return codes[idx]; }
 
+// Cache policy of the decode kernels' weight loads: non-temporal.  A forward
+// reads every weight once, so streaming them with this hint keeps them from
+// displacing x, y and the partial sums in L2 and the last-level cache (the
+// tiled kernel keeps ordinary loads: the row blocks of a column block reuse
+// its weights from L2).
+constexpr int kWeightPolicy = 2;   // cache-policy operand of the buffer builtins: nt
+__device__ inline uint4 load_block_nt(const uint4 *codes, size_t idx) {
+    return __builtin_bit_cast(uint4, __builtin_nontemporal_load((const v4u *)codes + idx));
+}
+
 // Per (column, group) dequantization word: bf16 s in the low half and the
 // bf16 offset zc = -(128 + z) in the high half (exact: an integer of 8
 // significant bits), so that (128 + q) * s + zc * s = (q - z) * s.
@@ -92,18 +102,12 @@ __device__ inline uint32_t load_sz(const void *sz, size_t idx) {
     }
 }
 
-// The same two loads for block b (wave-uniform) and lane l: the block's base
-// address is formed once in scalar registers, so each load is a scalar base
-// plus the lane's 32-bit offset, with no 64-bit vector address arithmetic.
-__device__ inline uint4 load_block_at(const uint4 *codes, uint32_t b, int lane) {
-    return (codes + (size_t)b * 64)[lane];
-}
 template <bool SYM>
-__device__ inline uint32_t load_sz_at(const void *sz, uint32_t b, int col) {
+__device__ inline uint32_t load_sz_nt(const void *sz, size_t idx) {   // non-temporal, as load_block_nt
     if constexpr (SYM) {
-        return (uint32_t)((const uint16_t *)sz + (size_t)b * 16)[col] | (kZcSymmetric << 16);
+        return (uint32_t)__builtin_nontemporal_load((const uint16_t *)sz + idx) | (kZcSymmetric << 16);
     } else {
-        return ((const uint32_t *)sz + (size_t)b * 16)[col];
+        return __builtin_nontemporal_load((const uint32_t *)sz + idx);
     }
 }
 

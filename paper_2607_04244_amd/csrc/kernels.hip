@@ -409,12 +409,12 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     auto fetch = [&](int d, uint32_t u) {
         u = min(u, ulast);
         const uint32_t rb = u + tile_of(u) * skip;                // block relative to base
-        cb[d] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rcodes, lane * 16, rb * 1024, 0));
+        cb[d] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rcodes, lane * 16, rb * 1024, kWeightPolicy));
         if constexpr (SYM) {
-            sb[d] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rsz, lm * 2, rb * (kTileN * 2), 0) |
+            sb[d] = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(rsz, lm * 2, rb * (kTileN * 2), kWeightPolicy) |
                     (kZcSymmetric << 16);
         } else {
-            sb[d] = __builtin_amdgcn_raw_buffer_load_b32(rsz, lm * 4, rb * (kTileN * 4), 0);
+            sb[d] = __builtin_amdgcn_raw_buffer_load_b32(rsz, lm * 4, rb * (kTileN * 4), kWeightPolicy);
         }
     };
 #pragma unroll
@@ -622,8 +622,8 @@ __global__ void __launch_bounds__(kThreads) k_mfma16(FwdArgs a) {
 #pragma unroll
             for (int t = 0; t < TN; ++t) {
                 const size_t b = base + (size_t)min(max(t, ta), tb - 1) * a.Kb;
-                B.c[t] = load_block(a.codes, b * 64 + lane);
-                B.s[t] = load_sz<SYM>(a.sz, b * kTileN + lm);
+                B.c[t] = load_block_nt(a.codes, b * 64 + lane);
+                B.s[t] = load_sz_nt<SYM>(a.sz, b * kTileN + lm);
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) B.x[j] = load_xfrag(a, w.g0 + kbl, j, lane);
@@ -696,13 +696,13 @@ __global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
 #pragma unroll
             for (int t = 0; t < TN; ++t) {
                 const size_t b = base + (size_t)min(max(t, ta), tb - 1) * a.Kb;
-                B.c[t] = load_block(a.codes, b * 64 + lane);
+                B.c[t] = load_block_nt(a.codes, b * 64 + lane);
                 if constexpr (SYM) {
-                    const uint2 h = *(const uint2 *)((const uint16_t *)a.sz + b * kTileN + 4 * b2);
+                    const uint2 h = __builtin_bit_cast(uint2, __builtin_nontemporal_load((const v2u *)((const uint16_t *)a.sz + b * kTileN + 4 * b2)));
                     B.s[t] = make_uint4((h.x & 0xFFFFu) | (kZcSymmetric << 16), (h.x >> 16) | (kZcSymmetric << 16),
                                         (h.y & 0xFFFFu) | (kZcSymmetric << 16), (h.y >> 16) | (kZcSymmetric << 16));
                 } else {
-                    B.s[t] = *(const uint4 *)((const uint32_t *)a.sz + b * kTileN + 4 * b2);
+                    B.s[t] = __builtin_bit_cast(uint4, __builtin_nontemporal_load((const v4u *)((const uint32_t *)a.sz + b * kTileN + 4 * b2)));
                 }
             }
 #pragma unroll
