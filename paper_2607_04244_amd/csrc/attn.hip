@@ -143,8 +143,8 @@ __global__ __launch_bounds__(kSplitWaves * 64, 1) void k_attn_split(AttnArgs a) 
         for (int j = 0; j < 2; ++j) {
             const int u = (kSplitWaves * j + wave) * 64 + lane;
             const int kk = u >> 4, c = (u & 15) ^ (kk & 15), key = min(key0 + kk, a.hi - 1);
-            load_lds_x16(kh + (size_t)key * kAttnD + 8 * c, &kring[st][(kSplitWaves * j + wave) * 64]);
-            load_lds_x16(vh + (size_t)key * kAttnD + 8 * c, &vring[st][(kSplitWaves * j + wave) * 64]);
+            load_lds_x16_nt(kh + (size_t)key * kAttnD + 8 * c, &kring[st][(kSplitWaves * j + wave) * 64]);
+            load_lds_x16_nt(vh + (size_t)key * kAttnD + 8 * c, &vring[st][(kSplitWaves * j + wave) * 64]);
         }
     };
     for (int t = t0; t < min(t0 + NS, t1); ++t) issue(t);

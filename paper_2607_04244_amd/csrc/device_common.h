@@ -205,6 +205,12 @@ __device__ inline void load_lds_x16(const void *src, const uint4 *lds_dst) {
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" :: "s"(m0), "v"(src) : "memory", "m0");
 }
 
+// The same with the non-temporal hint, for data a call reads once.
+__device__ inline void load_lds_x16_nt(const void *src, const uint4 *lds_dst) {
+    const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds_dst);
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off nt" :: "s"(m0), "v"(src) : "memory", "m0");
+}
+
 // The same with 4 bytes per lane: lane l's dword lands at lds_dst + 4 l.
 __device__ inline void load_lds_x4(const void *src, const void *lds_dst) {
     const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds_dst);
