@@ -15,7 +15,7 @@ constexpr int kBlockU32 = 256;     // packed words per (16 n x 128 k) block = 1 
 #define QLIN_WAVES 8
 #endif
 #ifndef QLIN_DEPTH
-#define QLIN_DEPTH 4
+#define QLIN_DEPTH 3
 #endif
 constexpr int kWaves = QLIN_WAVES; // waves per workgroup of the forward kernels
 constexpr int kDepth = QLIN_DEPTH; // 1 KiB weight blocks in flight per wave
