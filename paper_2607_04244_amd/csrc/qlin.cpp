@@ -293,6 +293,7 @@ double plan_cost(const qlin_s *h, int kern, int M, int S, int Gn) {
 // weight copies) at M = 1, 2, 4, 8, 12 .. 16, and these won by 4-12%.
 struct TunedPlan { int m_lo, m_hi, K, N, kern, S; };
 constexpr TunedPlan kTunedPlans[] = {
+    {1, 2, 2560, 19456, kKernStaged, 1},    // gate|up at one or two rows (20% ahead of the register kernel)
     {13, 16, 2560, 1024, kKernStaged, 1},   // k and v projections
     {13, 16, 2560, 2560, kKernStaged, 1},
     {13, 16, 2560, 4096, kKernStaged, 1},   // q projection

@@ -402,6 +402,7 @@ def test_forward_argument_errors():
 
 @pytest.mark.parametrize("M,K,N,kernel,split", [
     (16, 2560, 19456, "k_skinny<1,16>", 1),    # the draft-block verification linear
+    (1, 2560, 19456, "k_skinny<1,1>", 1),      # gate|up at one row (measured plan)
     (16, 2560, 6144, "k_skinny<1,16>", 1),     # q|k|v of a layer
     (16, 4096, 2560, "k_skinny<1,16>", 1),     # o projection (measured plan)
     (16, 9728, 2560, "k_skinny<1,16>", 3),     # down projection (measured plan)
