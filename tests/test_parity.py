@@ -343,6 +343,27 @@ def test_extreme_shapes():
         lin.close()
 
 
+def test_maximum_sizes():
+    # the largest N and M the boundary accepts: N = 2^20 columns (65536 column
+    # tiles, a 64 MiB code array; checked on sampled columns, each of which
+    # the oracle computes from its own weights alone), and M = 65536 rows
+    # through the tiled kernel
+    K, N, M = 128, 1 << 20, 3
+    c = gen.random_case(K + N, M, K, N)
+    lin = make(c)
+    y = run(lin, c["x"])
+    lin.close()
+    rng = np.random.default_rng(5)
+    cols = np.unique(np.concatenate([np.arange(256), np.arange(N - 256, N), rng.integers(0, N, 1024)]))
+    y_ref = ref.forward(c["x"], c["packed"][cols], c["scales"][cols], c["zeros"][cols])
+    assert_close(np.ascontiguousarray(y[:, cols]), y_ref, f"K={K} N={N} M={M} sampled columns")
+    K, N, M = 256, 64, 65536
+    c = gen.random_case(K + N + M, M, K, N)
+    lin = make(c)
+    assert_close(run(lin, c["x"]), oracle(c), f"K={K} N={N} M={M}")
+    lin.close()
+
+
 def test_zero_rows_is_a_noop_and_repeat_calls_agree():
     c = gen.random_case(9, 16, 1280, 160)
     lin = make(c)
