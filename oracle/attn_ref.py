@@ -15,7 +15,7 @@ What it computes (Kim, Lee, Kim, arXiv 2607.04244):
   cache stays complete; sequences no longer than the window use full
   attention.
 
-Readings taken where the paper is silent (each is listed in the design doc):
+Readings taken where the paper is silent:
 
 * The 16 queries of the block sit at the last 16 positions of the cache:
   query i (0 <= i < 16) is at position p_i = T - 16 + i of the T cached keys.

@@ -15,7 +15,7 @@ arXiv 2607.04244):
   into floating point (BF16 weights), so the matmul sees bf16 weights.
 * Sec. 3.3 (Drafter PTQ): group-wise INT4 with a group size of 128 along K.
 
-Readings taken where the paper is silent (each is listed in the design doc):
+Readings taken where the paper is silent:
 
 * Codes are unsigned 4-bit q in [0, 15] with a per-group zero-point z, so the
   signed code of the paper is W_q = q - z.  The paper's symmetric format is the
