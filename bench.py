@@ -340,7 +340,7 @@ def main():
     ap.add_argument("--fuse-qkv", action="store_true", help="model / prefill passes: one q|k|v launch per layer")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the layer has no multi-GPU path in this build "
+        print("bench.py measures one GPU: the layer has no multi-GPU path in this library "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
     if args.calibrate_copy:

@@ -39,7 +39,7 @@ typedef struct qlin_s *qlin_t;   /* opaque; immutable after creation */
 enum {
     QLIN_OK = 0,
     QLIN_ERR_INVALID = -1,      /* bad argument (size, NULL, aliasing, zero-point value) */
-    QLIN_ERR_UNSUPPORTED = -2,  /* valid but outside this build (group != 128, N % 16, scale range, M) */
+    QLIN_ERR_UNSUPPORTED = -2,  /* valid but outside this library (group != 128, N % 16, scale range, M) */
     QLIN_ERR_ALIGN = -3,        /* x or y not 16-byte aligned */
     QLIN_ERR_OOM = -4,          /* device allocation failed */
     QLIN_ERR_HIP = -5           /* a HIP runtime call or kernel launch failed */

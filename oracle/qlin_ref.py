@@ -161,7 +161,7 @@ def quantize_rtn(w_bits, scales, zeros, group=GROUP):
     rounded back onto the quantization grid of the frozen scales, giving new
     4-bit codes under the same scales; Sec. 4 (drafter PTQ, Table of drafter
     quantizers): round-to-nearest is the RTN baseline.  With the unsigned
-    codes of this build (signed code = q - z):
+    codes of this library (signed code = q - z):
 
         code[n][k] = clamp(round(w[n][k] / s[n][g]) + z[n][g], 0, 15),  g = k // group
 
