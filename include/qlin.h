@@ -131,8 +131,8 @@ int qlin_forward(qlin_t h, int64_t M, const uint16_t *x, uint16_t *y, void *stre
  * K-chunks (split_k; 0 = the planner's choice) forced, for tests and tuning.
  * Errors as qlin_forward, plus INVALID for an unknown path, split_k < 0 or
  * split_k > K/128, and UNSUPPORTED when the path cannot run this M
- * (GEMV: M <= 4; REGS: M <= 16; SKINNY: M <= 64) or the forced split does
- * not fit.
+ * (GEMV: M <= 4; REGS: M <= 16; TILED: M * K < 2^31; SKINNY takes any M,
+ * in launches of up to 64 rows) or the forced split does not fit.
  */
 int qlin_forward_path(qlin_t h, int path, int64_t split_k, int64_t M,
                       const uint16_t *x, uint16_t *y, void *stream);
@@ -140,8 +140,8 @@ int qlin_forward_path(qlin_t h, int path, int64_t split_k, int64_t M,
 /*
  * qlin_plan -- describe, without launching, what qlin_forward_path would run
  * for (path, split_k, M): writes a NUL-terminated text such as
- * "path=skinny kernel=qlin_skinny_mt1 grid=256 block=512 split=1 lds=88064"
- * into buf (at most buflen bytes).  Returns QLIN_OK or an error as
+ * "path=skinny kernel=k_skinny<1,16> grid=256 block=512 split=1 ranges=256
+ * lds=123904 launches=1" into buf (at most buflen bytes).  Returns QLIN_OK or an error as
  * qlin_forward_path.
  */
 int qlin_plan(qlin_t h, int path, int64_t split_k, int64_t M, char *buf, int64_t buflen);
