@@ -77,6 +77,8 @@ def check(q, k, v, T, W, splits=0, what=""):
     (8, 2, 5, 400, 128),        # ragged block: 5 queries
     (2, 1, 1, 1, 0),            # one token
     (2, 1, 16, 16, 0),          # cache = the block
+    (8, 2, 16, 600, 101),       # odd window: half window 50 on each side
+    (8, 2, 16, 257, 256),       # cache one token longer than the window
 ])
 def test_matches_oracle(Hq, Hkv, nq, T, W):
     q, k, v = case(Hq, Hkv, nq, T, seed=T + W)
