@@ -91,3 +91,22 @@ def test_grouped_heads_read_their_kv_head():
     qp = q.reshape(Hkv, 2, 16, 128)[perm].reshape(Hq, 16, 128)
     outp = ar.swa_attention(qp, k[perm], v[perm], 32)
     assert np.array_equal(outp.reshape(Hkv, 2, 16, 128), out.reshape(Hkv, 2, 16, 128)[perm])
+
+
+def test_two_keys_closed_form_fixes_the_score_scale():
+    """Scores are q.k / sqrt(128): the standard scaled dot-product attention
+    the drafter of Sec. 2.3 uses, whose scale the paper does not spell out
+    (a reading; head dimension 128).  One query, two keys: q = 7.84375 e0 (exact in bf16),
+    k0 = e0, k1 = 0, so the scores are 7.84375 / sqrt(128) = 0.693296 (ln 2 +
+    1.5e-4) and 0; with v0 = 1, v1 = 0 every output element is
+    e^s / (e^s + 1) = 2/3 + 3.31e-5.  A missing or different scale gives
+    0.9996 (none), 0.727 (1/8) or 0.515 (1/128)."""
+    D = 128
+    q = np.zeros((1, 1, D))
+    q[0, 0, 0] = 7.84375
+    k = np.zeros((1, 2, D))
+    k[0, 0, 0] = 1.0
+    v = np.zeros((1, 2, D))
+    v[0, 0, :] = 1.0
+    out = ar.swa_attention(_bf16(q), _bf16(k), _bf16(v), 0)
+    assert np.all(np.abs(out - (2.0 / 3.0 + 3.31e-5)) < 1e-6)
