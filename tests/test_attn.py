@@ -102,6 +102,26 @@ def test_cache_capacity_beyond_T_is_not_read():
             check(q, k, v, T, W, splits=splits, what=f"capacity W={W} splits={splits}")
 
 
+def test_heads_beyond_two_gib_of_cache():
+    """kv_stride = 2^23 tokens: key/value head 1 starts 2 GiB into each cache
+    (byte offsets past 2^31); only the first T tokens of a head are filled."""
+    T, W, cap = 300, 64, 1 << 23
+    q, k, v = case(4, 2, 16, T, seed=11)
+    kt = torch.zeros((2, cap, 128), dtype=torch.bfloat16, device="cuda")
+    vt = torch.zeros((2, cap, 128), dtype=torch.bfloat16, device="cuda")
+    kt[:, :T] = dev(k)
+    vt[:, :T] = dev(v)
+    for splits in (0, 3):
+        out = qlin.swa_attention(dev(q), kt, vt, W, T=T, splits=splits)
+        torch.cuda.synchronize()
+        got = host_f64(out)
+        ref = ar.swa_attention(q, k, v, W)
+        bad = np.abs(got - ref) > tolerance(q, k, v, T, W, ref)
+        assert not bad.any(), f"splits={splits}: {bad.sum()} outside tolerance"
+    del kt, vt
+    torch.cuda.empty_cache()
+
+
 def test_window_of_one_returns_the_own_value_row_exactly():
     """W = 1: half window 0, each query sees only its own key (weight 1)."""
     T, nq = 200, 16
