@@ -364,6 +364,22 @@ def test_maximum_sizes():
     lin.close()
 
 
+def test_code_array_beyond_two_gib():
+    # K = 65536 (the largest), N = 69632: 2.28 GB of codes, so column tiles
+    # past 2 GiB are addressed; checked on sampled columns
+    K, N = 65536, 69632
+    c = gen.random_case(3, 16, K, N)
+    lin = make(c)
+    rng = np.random.default_rng(9)
+    cols = np.unique(np.concatenate([np.arange(64), np.arange(N - 64, N), rng.integers(0, N, 256)]))
+    for M in (1, 16):
+        x = c["x"][:M]
+        y = run(lin, x)
+        y_ref = ref.forward(x, c["packed"][cols], c["scales"][cols], c["zeros"][cols])
+        assert_close(np.ascontiguousarray(y[:, cols]), y_ref, f"K={K} N={N} M={M} sampled columns")
+    lin.close()
+
+
 def test_zero_rows_is_a_noop_and_repeat_calls_agree():
     c = gen.random_case(9, 16, 1280, 160)
     lin = make(c)
