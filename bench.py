@@ -16,19 +16,25 @@ byte count (qlin_stream_read), the achievable ceiling at this size.
 
 Prints one JSON line.  ``value`` is algorithmic bytes per step / time per step
 (GB/s); the algorithmic bytes are the int4 codes, the bf16 scales and zeros,
-x and y (K*N/2 + 4*(K/128)*N + 2*M*K + 2*M*N).
+x and y (K*N/2 + 4*(K/128)*N + 2*M*K + 2*M*N).  ``metric_parts`` carries the
+rest of the metric, measured in the same run: the M=1 linear (K=N=2560,
+GB/s) and the 36-layer 4B-shaped weight pass at M=16 (microseconds per
+verification step and per layer: q|k|v as one grouped launch, then o,
+gate|up and down, 144 launches in one graph on one stream, so each runs after
+the previous one as in a decoder), and the drafter's 5-layer pass.
 
 Other modes (not the benchmark line): ``--workload`` c0 | c2m1 | c2m4 |
-c2m8 | c2m16 | model (36 layers x 6 linears at M=16, microseconds per
-verification step) | prefill128 | prefill512 | prefill2048 (the same linears
-at M rows, TFLOP/s and matrix-core utilisation) | quantize (bf16 -> packed
-int4 codes on a fixed grid, GB/s) | swa1024 | swa2048 | attn-full |
-attn-short (the drafter's block attention: 32 query heads over 8 key/value
-heads of dimension 128, 16 block queries, a T = 8192 cache with a symmetric
-window of 1024 or 2048 tokens, full attention, and T = 700 inside the
-window; GB/s of the visible key/value span); ``--fuse-qkv`` runs the
-q, k, v projections of a layer as one launch; ``--calibrate-copy`` runs a
-plain 256 MiB device copy for the HBM-traffic counter calibration.
+c2m8 | c2m16 | model (the 36-layer pass at M=16) | drafter (the drafter's
+five layers and context projection at M=16, symmetric format) | prefill128
+| prefill512 | prefill2048 (the 36-layer linears at M rows, TFLOP/s and
+matrix-core utilisation) | quantize (bf16 -> packed int4 codes on a fixed
+grid, GB/s) | swa1024 | swa2048 | attn-full | attn-short (the drafter's
+block attention: 32 query heads over 8 key/value heads of dimension 128, 16
+block queries, a T = 8192 cache with a symmetric window of 1024 or 2048
+tokens, full attention, and T = 700 inside the window; GB/s of the visible
+key/value span); ``--separate-qkv`` runs q, k and v as three launches;
+``--calibrate-copy`` runs a plain 256 MiB device copy for the HBM-traffic
+counter calibration.
 """
 
 import argparse
@@ -94,26 +100,44 @@ def traffic_from_profiles(kernel, key=None):
     return e.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(case, budget_s=12.0):
-    """Time the oracle (as it stands) on the host cores on whole calls."""
-    from oracle import qlin_ref as ref
+def host_cores():
+    """Cores this process may run on (its affinity mask)."""
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
+def cpu_baseline(case, budget_s=12.0):
+    """Time the oracle (as it stands) on the host cores on whole calls, with
+    the BLAS threads set to the cores of the affinity mask; the unpack +
+    dequantize step is also timed on its own (the rest is the fp64 matmul)."""
+    from oracle import qlin_ref as ref
+    cores = host_cores()
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=cores, user_api="blas")
     except Exception:
-        threads = 1
-    times = []
+        limiter = None
+    times, deq = [], []
     t_start = time.perf_counter()
     while time.perf_counter() - t_start < budget_s and len(times) < 50:
         t0 = time.perf_counter()
         ref.forward(case["x"], case["packed"], case["scales"], case["zeros"])
         times.append(time.perf_counter() - t0)
-    t = float(np.median(times))
+        if len(deq) < 3:
+            t0 = time.perf_counter()
+            ref.dequant_bf16(case["packed"], case["scales"], case["zeros"])
+            deq.append(time.perf_counter() - t0)
+    if limiter is not None:
+        limiter.unregister()
+    t, td = float(np.median(times)), float(np.median(deq))
     b = algorithmic_bytes(case["M"], case["K"], case["N"])
-    return {"value": round(b / t / 1e9, 4), "unit": "GB/s", "cores": int(threads), "kind": "oracle",
+    return {"value": round(b / t / 1e9, 4), "unit": "GB/s", "cores": int(cores), "kind": "oracle",
             "sample": f"{len(times)} whole oracle calls of the M={case['M']} K={case['K']} N={case['N']} "
-                      f"linear (median {t:.3f} s each; numpy unpack/dequant single-threaded, fp64 "
-                      f"matmul on {threads} BLAS threads)"}
+                      f"linear (median {t:.3f} s each: unpack + dequantize {td:.3f} s in numpy, one thread; "
+                      f"fp64 matmul {max(t - td, 0.0):.3f} s on up to {cores} BLAS threads)",
+            "unpack_dequant_s": round(td, 4), "matmul_s": round(max(t - td, 0.0), 4)}
 
 
 def graph_time_us(torch, stream, launches, reps):
@@ -185,45 +209,72 @@ def calibrate_copy():
                       "bytes_written_per_launch": 1 << 28, "launches": 20}), flush=True)
 
 
-def bench_model(args, M=16, x_seed=3, fuse_qkv=False):
-    """36 layers x (q, k, v, o, gate_up, down) at M rows: one graph per step.
-    With fuse_qkv the q, k and v weights of a layer are concatenated along N
-    into one handle (the three share their input), so a layer takes four
-    launches instead of six; the outputs are the same columns."""
+def model_pass(M=16, x_seed=3, separate_qkv=False, drafter=False, reps=15):
+    """The linears of a whole decoder step at M rows, one graph on one stream:
+    per layer q|k|v (one grouped launch, or three), o, gate|up, down.  The
+    target: 36 layers of config-3 weights (asymmetric).  The drafter: its 5
+    layers and its context projection (symmetric, Sec. 3.3).  Prefill-sized
+    M share one caller workspace sized for the largest plan.  Returns a dict
+    of the step time and rates."""
     import torch
 
     from paper_2607_04244_amd import qlin
     from synth import gen
     torch.cuda.set_device(0)
-    lins, xs, ys, total, flops = [], {}, [], 0, 0
-    for layer in range(gen.N_LAYERS):
-        ws = [gen.model_linear(layer, p) for p in range(len(gen.LAYER_SHAPES))]
-        if fuse_qkv:
-            qkv = dict(K=ws[0]["K"], N=sum(w["N"] for w in ws[:3]),
-                       packed=np.concatenate([w["packed"] for w in ws[:3]]),
-                       scales=np.concatenate([w["scales"] for w in ws[:3]]),
-                       zeros=np.concatenate([w["zeros"] for w in ws[:3]]))
-            ws = [qkv] + ws[3:]
-        for w in ws:
-            lins.append(qlin.QLinear(w["packed"], w["scales"], w["zeros"]))
-            K, N = w["K"], w["N"]
-            if K not in xs:
-                xs[K] = torch.from_numpy(gen.model_activations(x_seed, M, K).view(np.int16)).view(torch.bfloat16).cuda()
-            ys.append(torch.empty((M, N), dtype=torch.bfloat16, device="cuda"))
-            total += algorithmic_bytes(M, K, N)
-            flops += 2 * M * K * N
+    n_layers = gen.DRAFTER_LAYERS if drafter else gen.N_LAYERS
+    layers, xs, total, flops = [], {}, 0, 0
+    t0 = time.perf_counter()
+    for layer in range(n_layers):
+        if drafter:
+            ws = [gen.drafter_linear(layer, p) for p in range(len(gen.LAYER_SHAPES))]
+            lins = [qlin.QLinear(w["packed"], w["scales"], None) for w in ws]
+        else:
+            ws = [gen.model_linear(layer, p) for p in range(len(gen.LAYER_SHAPES))]
+            lins = [qlin.QLinear(w["packed"], w["scales"], w["zeros"]) for w in ws]
+        groups = [[l] for l in lins[:3]] if separate_qkv else [lins[:3]]
+        groups += [[l] for l in lins[3:]]
+        layers.extend(groups)
+    if drafter:
+        w = gen.drafter_linear(0, len(gen.LAYER_SHAPES))
+        layers.insert(0, [qlin.QLinear(w["packed"], w["scales"], None)])
+    setup_s = time.perf_counter() - t0
+    steps = []
+    for grp in layers:
+        K = grp[0].K
+        if K not in xs:
+            xs[K] = torch.from_numpy(gen.model_activations(x_seed, M, K).view(np.int16)).view(torch.bfloat16).cuda()
+        ys = [torch.empty((M, l.N), dtype=torch.bfloat16, device="cuda") for l in grp]
+        steps.append((grp, ys))
+        for l in grp:
+            total += algorithmic_bytes(M, K, l.N, symmetric=drafter)
+            flops += 2 * M * K * l.N
+    need = max(qlin.group_plan(grp, M)[0] for grp, _ in steps)
+    wsb = qlin.new_workspace(need) if need else None
     stream = torch.cuda.Stream()
-    calls = [(lambda l=l, y=y: l.forward(xs[l.K], out=y)) for l, y in zip(lins, ys)]
-    us_per_launch, g = graph_time_us(torch, stream, calls, reps=max(1, args.steps // len(calls)))
+    calls = [(lambda grp=grp, ys=ys: qlin.forward_group(grp, xs[grp[0].K], ys, workspace=wsb)) for grp, ys in steps]
+    us_per_launch, g = graph_time_us(torch, stream, calls, reps=reps)
     us_step = us_per_launch * len(calls)
     tfs = flops / (us_step * 1e-6) / 1e12
-    out = {"workload": f"36-layer 4B decoder weight pass M={M} ({len(calls)} launches"
-                       f"{', fused qkv' if fuse_qkv else ''}, one graph)",
-           "us_per_step": round(us_step, 2), "us_per_layer": round(us_step / gen.N_LAYERS, 3),
-           "bytes_per_step": total, "GBps": round(total / (us_step * 1e-6) / 1e9, 1),
-           "pct_of_peak_hbm": round(100 * total / (us_step * 1e-6) / 1e9 / PEAK_HBM_GBS, 2),
-           "TFLOPs": round(tfs, 1), "mfma_util_pct": round(100 * tfs / PEAK_BF16_TFLOPS, 2),
-           "plans": sorted({l.plan(M) for l in lins})}
+    gbs = total / (us_step * 1e-6) / 1e9
+    plans = sorted({qlin.group_plan(grp, M)[1] for grp, _ in steps})
+    del g
+    for grp, _ in steps:
+        for l in grp:
+            l.close()
+    torch.cuda.empty_cache()
+    who = (f"drafter: {n_layers} layers + context projection, symmetric" if drafter
+           else f"36-layer 4B decoder weight pass")
+    return {"workload": f"{who}, M={M} ({len(calls)} launches, "
+                        f"{'separate' if separate_qkv else 'grouped'} q|k|v, one graph)",
+            "us_per_step": round(us_step, 2), "us_per_layer": round(us_step / n_layers, 3),
+            "bytes_per_step": total, "GBps": round(gbs, 1), "pct_of_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2),
+            "TFLOPs": round(tfs, 1), "mfma_util_pct": round(100 * tfs / PEAK_BF16_TFLOPS, 2),
+            "workspace_bytes": need, "setup_s": round(setup_s, 1), "plans": plans}
+
+
+def bench_model(args, M=16, x_seed=3, drafter=False):
+    out = model_pass(M, x_seed, separate_qkv=args.separate_qkv, drafter=drafter,
+                     reps=max(5, min(50, args.steps // 144)))
     print(json.dumps(out), flush=True)
 
 
@@ -315,16 +366,92 @@ def bench_attention(args, name):
             ar.swa_attention(c["q"], c["k"], c["v"], W)
             times.append(time.perf_counter() - t0)
         t = float(np.median(times))
-        try:
-            from threadpoolctl import threadpool_info
-            threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-        except Exception:
-            threads = 1
+        threads = host_cores()
         res["cpu_baseline"] = {"value": round(nbytes / t / 1e9, 4), "unit": "GB/s", "cores": int(threads),
                                "kind": "oracle",
                                "sample": f"{len(times)} whole oracle calls (median {t:.3f} s; float64 numpy, "
-                                         f"matmuls on {threads} BLAS threads)"}
+                                         f"matmuls on up to {threads} BLAS threads)"}
     print(json.dumps(res), flush=True)
+
+
+def linear_rate(case, steps, warmup, path=0, split=0):
+    """Time `steps` forwards of one linear (HIP-graph replays over R handles
+    with their own weight copies, > 1 GiB together, so the weights come from
+    HBM), after `warmup` untimed ones; the timed region is bracketed by
+    device synchronisations.  Returns a dict of the rates and the plan."""
+    import torch
+
+    from paper_2607_04244_amd import qlin
+    M, K, N = case["M"], case["K"], case["N"]
+    bytes_step = algorithmic_bytes(M, K, N)
+    weight_bytes = K * N // 2 + 4 * (K // 128) * N
+    R = max(2, -(-(1 << 30) // weight_bytes))          # > 1 GiB of distinct weights
+    lins = [qlin.QLinear(case["packed"], case["scales"], case["zeros"]) for _ in range(R)]
+    x = torch.from_numpy(case["x"].view(np.int16)).view(torch.bfloat16).cuda()
+    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    # a forced split or tiled path runs with a caller workspace of its size
+    ws = None
+    if split or path == qlin.PATH_TILED:
+        need, plan = qlin.group_plan([lins[0]], M, path, split)
+        ws = qlin.new_workspace(need) if need else None
+    else:
+        plan = lins[0].plan(M, path, split)
+
+    stream = torch.cuda.Stream()
+    with torch.cuda.stream(stream):
+        for i in range(warmup):
+            lins[i % R].forward(x, out=y, path=path, split_k=split, workspace=ws)
+    stream.synchronize()
+
+    # one graph of R steps (every weight copy once); the steps = whole replays + a tail graph
+    def capture(n):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            for i in range(n):
+                lins[i % R].forward(x, out=y, path=path, split_k=split, workspace=ws)
+        return g
+
+    g_full = capture(R)
+    tail = steps % R
+    g_tail = capture(tail) if tail else None
+    with torch.cuda.stream(stream):
+        for _ in range(2):
+            g_full.replay()
+    stream.synchronize()
+
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        ev0.record(stream)
+        for _ in range(steps // R):
+            g_full.replay()
+        if g_tail is not None:
+            g_tail.replay()
+        ev1.record(stream)
+    stream.synchronize()
+    torch.cuda.synchronize()
+    ms_step = ev0.elapsed_time(ev1) / steps
+    gbs = bytes_step / (ms_step * 1e-3) / 1e9
+
+    # eager launches from Python, for reference (host-launch bound for small kernels)
+    ev2 = torch.cuda.Event(enable_timing=True)
+    ev3 = torch.cuda.Event(enable_timing=True)
+    n_eager = min(steps, 2000)
+    with torch.cuda.stream(stream):
+        ev2.record(stream)
+        for i in range(n_eager):
+            lins[i % R].forward(x, out=y, path=path, split_k=split, workspace=ws)
+        ev3.record(stream)
+    stream.synchronize()
+    eager_us = ev2.elapsed_time(ev3) * 1e3 / n_eager
+    del g_full, g_tail
+    for l in lins:
+        l.close()
+    del lins
+    torch.cuda.empty_cache()
+    return {"ms_step": ms_step, "GBps": gbs, "plan": plan, "R": R, "bytes": bytes_step, "eager_us": eager_us,
+            "stream": stream}
 
 
 def main():
@@ -333,11 +460,12 @@ def main():
     ap.add_argument("--steps", type=int, default=4000)
     ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle timing")
+    ap.add_argument("--no-parts", action="store_true", help="skip the M=1, model and drafter passes")
     ap.add_argument("--path", type=int, default=0, help="force a kernel path (tuning)")
     ap.add_argument("--split", type=int, default=0, help="force a K split (tuning)")
     ap.add_argument("--workload", default="verify")
     ap.add_argument("--calibrate-copy", action="store_true")
-    ap.add_argument("--fuse-qkv", action="store_true", help="model / prefill passes: one q|k|v launch per layer")
+    ap.add_argument("--separate-qkv", action="store_true", help="model / prefill passes: q, k, v as three launches")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the layer has no multi-GPU path in this library "
@@ -347,9 +475,11 @@ def main():
         return calibrate_copy()
     if args.workload.startswith("prefill"):
         # chunked-prefill regime: M rows through every linear of the model
-        return bench_model(args, M=int(args.workload[len("prefill"):]), x_seed=4, fuse_qkv=args.fuse_qkv)
+        return bench_model(args, M=int(args.workload[len("prefill"):]), x_seed=4)
     if args.workload == "model":
-        return bench_model(args, fuse_qkv=args.fuse_qkv)
+        return bench_model(args)
+    if args.workload == "drafter":
+        return bench_model(args, drafter=True)
     if args.workload == "quantize":
         return bench_quantize(args)
     if args.workload in ATTN_WORKLOADS:
@@ -362,69 +492,29 @@ def main():
     torch.cuda.set_device(0)
     case = make_case(args.workload)
     M, K, N = case["M"], case["K"], case["N"]
-    bytes_step = algorithmic_bytes(M, K, N)
-    weight_bytes = K * N // 2 + 4 * (K // 128) * N
-    R = max(2, -(-(1 << 30) // weight_bytes))          # > 1 GiB of distinct weights
-    lins = [qlin.QLinear(case["packed"], case["scales"], case["zeros"]) for _ in range(R)]
-    x = torch.from_numpy(case["x"].view(np.int16)).view(torch.bfloat16).cuda()
-    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
-    plan = lins[0].plan(M, args.path, args.split)
-
-    stream = torch.cuda.Stream()
-    with torch.cuda.stream(stream):
-        for i in range(args.warmup):
-            lins[i % R].forward(x, out=y, path=args.path, split_k=args.split)
-    stream.synchronize()
-
-    # one graph of R steps (every weight copy once); K steps = whole replays + a tail graph
-    def capture(n):
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g, stream=stream):
-            for i in range(n):
-                lins[i % R].forward(x, out=y, path=args.path, split_k=args.split)
-        return g
-
+    r = linear_rate(case, args.steps, args.warmup, args.path, args.split)
+    ms_step, gbs, plan, R, bytes_step, eager_us = r["ms_step"], r["GBps"], r["plan"], r["R"], r["bytes"], r["eager_us"]
     K_steps = args.steps
-    g_full = capture(R)
-    tail = K_steps % R
-    g_tail = capture(tail) if tail else None
-    with torch.cuda.stream(stream):
-        for _ in range(2):
-            g_full.replay()
-    stream.synchronize()
+    ceil_gbs, ceil_us = stream_read_ceiling(torch, qlin, bytes_step, r["stream"])
 
-    ev0 = torch.cuda.Event(enable_timing=True)
-    ev1 = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    with torch.cuda.stream(stream):
-        ev0.record(stream)
-        for _ in range(K_steps // R):
-            g_full.replay()
-        if g_tail is not None:
-            g_tail.replay()
-        ev1.record(stream)
-    stream.synchronize()
-    torch.cuda.synchronize()
-    ms_total = ev0.elapsed_time(ev1)
-    ms_step = ms_total / K_steps
-    gbs = bytes_step / (ms_step * 1e-3) / 1e9
-
-    # eager launches from Python, for reference (host-launch bound for small kernels)
-    ev2 = torch.cuda.Event(enable_timing=True)
-    ev3 = torch.cuda.Event(enable_timing=True)
-    n_eager = min(K_steps, 2000)
-    with torch.cuda.stream(stream):
-        ev2.record(stream)
-        for i in range(n_eager):
-            lins[i % R].forward(x, out=y, path=args.path, split_k=args.split)
-        ev3.record(stream)
-    stream.synchronize()
-    eager_us = ev2.elapsed_time(ev3) * 1e3 / n_eager
-    for l in lins:
-        l.close()
-    del lins
-    torch.cuda.empty_cache()
-    ceil_gbs, ceil_us = stream_read_ceiling(torch, qlin, bytes_step, stream)
+    parts = None
+    if args.workload == "verify" and not args.no_parts:
+        # the rest of the metric: the M=1 linear, and microseconds per layer of
+        # the whole 4B-shaped step (and the drafter's) at M=16
+        print("measuring the M=1 linear and the model passes", file=sys.stderr, flush=True)
+        c0 = linear_rate(make_case("c0"), 2000, 100)
+        model = model_pass(16)
+        draft = model_pass(16, drafter=True)
+        parts = {"M1_K2560_N2560": {"us": round(c0["ms_step"] * 1e3, 3), "GBps": round(c0["GBps"], 1),
+                                    "pct_of_peak_hbm": round(100 * c0["GBps"] / PEAK_HBM_GBS, 2),
+                                    "plan": c0["plan"]},
+                 "M16_K2560_N19456": {"us": round(ms_step * 1e3, 3), "GBps": round(gbs, 1),
+                                      "pct_of_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2)},
+                 "model_M16": {k: model[k] for k in ("workload", "us_per_step", "us_per_layer", "GBps",
+                                                     "pct_of_peak_hbm", "bytes_per_step")},
+                 "drafter_M16": {k: draft[k] for k in ("workload", "us_per_step", "us_per_layer", "GBps",
+                                                       "pct_of_peak_hbm", "bytes_per_step")}}
+        parts["model_M16"]["us_at_70pct_of_peak"] = round(model["bytes_per_step"] / (0.7 * PEAK_HBM_GBS * 1e3), 1)
 
     kernel = plan.split("kernel=")[1].split()[0] if "kernel=" in plan else "?"
     traffic = traffic_from_profiles(kernel)
@@ -450,6 +540,7 @@ def main():
                    "stream_read_ceiling_GBps": round(ceil_gbs, 1), "stream_read_ceiling_us": round(ceil_us, 3),
                    "pct_of_stream_read_ceiling": round(100 * gbs / ceil_gbs, 1),
                    "eager_launch_us_per_step": round(eager_us, 3)},
+        "metric_parts": parts,
         "roofline": {"bound": "hbm", "kernel": kernel, "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
                      "traffic": traffic, "bytes_per_launch": bytes_step,

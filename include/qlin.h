@@ -63,8 +63,9 @@ enum {
  *   zeros     bf16 [N][K/group]; integer values in [0, 15]
  *   group     must be 128 (Sec. 3.3)
  * Each of the three may be host memory or device memory of the current
- * device (such as qlin_quantize's output); device scales and zero-points are
- * copied to the host for the checks.
+ * device (such as qlin_quantize's output, written on the default stream or
+ * complete); device scales and zero-points are copied to the host for the
+ * checks.
  *
  * Constraints: K > 0, N > 0, K % 128 == 0, N % 16 == 0, K <= 65536,
  * N <= 1048576.  The call copies and re-lays-out the weights into device
@@ -117,10 +118,13 @@ int qlin_quantize(int64_t K, int64_t N, int64_t group, const uint16_t *w, const 
  *   stream  hipStream_t to launch on; NULL = the default stream
  *
  * M = 0 is a no-op returning QLIN_OK.  0 < M <= 65536.  x and y must stay
- * valid until the stream's work completes.  The handle owns a small
- * workspace, so one handle must not run on two streams at the same time
- * (different handles are independent).  The device current at call time
- * must be the handle's device.
+ * valid until the stream's work completes.  The handle owns a workspace
+ * sized for the plans of M <= 16 (the decode regime: one draft block), so one
+ * handle must not run on two streams at the same time (different handles
+ * are independent).  Larger M run with plans that fit that workspace; the
+ * fastest plans for prefill-sized M take a caller workspace through
+ * qlin_forward_group.  The device current at call time must be the handle's
+ * device.
  * Errors: INVALID (NULL, M < 0, overlap, wrong device), UNSUPPORTED (M too
  * large), ALIGN, HIP.
  */
@@ -131,8 +135,8 @@ int qlin_forward(qlin_t h, int64_t M, const uint16_t *x, uint16_t *y, void *stre
  * K-chunks (split_k; 0 = the planner's choice) forced, for tests and tuning.
  * Errors as qlin_forward, plus INVALID for an unknown path, split_k < 0 or
  * split_k > K/128, and UNSUPPORTED when the path cannot run this M
- * (GEMV: M <= 4; REGS: M <= 16; TILED: M * K < 2^31; SKINNY takes any M,
- * in launches of up to 64 rows) or the forced split does not fit.
+ * (GEMV: M <= 4; REGS: M <= 16; SKINNY: M <= 64; TILED: M * K < 2^31) or
+ * the forced split does not fit LDS or the handle's workspace.
  */
 int qlin_forward_path(qlin_t h, int path, int64_t split_k, int64_t M,
                       const uint16_t *x, uint16_t *y, void *stream);
@@ -146,7 +150,57 @@ int qlin_forward_path(qlin_t h, int path, int64_t split_k, int64_t M,
  */
 int qlin_plan(qlin_t h, int path, int64_t split_k, int64_t M, char *buf, int64_t buflen);
 
-/* qlin_destroy -- wait for the device to finish the handle's work, free it. NULL-safe. */
+/*
+ * qlin_forward_group -- y_i[M][N_i] = x[M][K] . w_i^T for the n handles hs[i]
+ * that share the input x: one launch of the decode kernels covers all of
+ * them (M <= 64), e.g. the q, k and v projections of a decoder layer, which
+ * the target runs on every verification step (Sec. 2.2) and the drafter on
+ * every drafting step (Sec. 2.3).  For M > 64 (or path TILED) the members run
+ * as consecutive tiled launches.  n = 1 is a forward of one handle with a
+ * caller workspace.
+ *
+ *   n          1 <= n <= 8 handles, all with the same K, the same format
+ *              (zero-points or symmetric) and on the current device
+ *   path, split_k   as qlin_forward_path (QLIN_PATH_AUTO, 0: the planner's)
+ *   x          DEVICE bf16 [M][K], 16-byte aligned
+ *   ys         HOST array of n DEVICE pointers, ys[i] bf16 [M][N_i],
+ *              16-byte aligned; no output may overlap x, another output or
+ *              the workspace
+ *   workspace  DEVICE memory of workspace_bytes (16-byte aligned), or NULL
+ *              with 0 bytes.  It must be zero-filled before its first use;
+ *              every call leaves it in a state the next call can use, so
+ *              one workspace can serve any handles and plans in stream
+ *              order (calls sharing one must not overlap in time).  The
+ *              planner picks the fastest plan whose K split fits it;
+ *              qlin_group_plan reports the size the unconstrained plan uses.
+ *   stream     hipStream_t; NULL = the default stream
+ * Asynchronous.  M = 0 is a no-op.
+ * Errors: INVALID (n, NULL, overlaps, K / format / device mismatch, sizes),
+ * UNSUPPORTED (as qlin_forward_path), ALIGN, HIP.
+ */
+int qlin_forward_group(int64_t n, const qlin_t *hs, int path, int64_t split_k, int64_t M, const uint16_t *x,
+                       uint16_t *const *ys, void *workspace, int64_t workspace_bytes, void *stream);
+
+/*
+ * qlin_group_plan -- without launching: the plan qlin_forward_group would run
+ * for (n, hs, path, split_k, M) with a workspace of workspace_bytes bytes
+ * (< 0: no limit), as text in buf (see qlin_plan; buf may be NULL), and in
+ * *workspace_needed (may be NULL) the workspace bytes that plan uses (0 when
+ * it does not cut the K range).  With workspace_bytes < 0 that is the size
+ * to allocate for the fastest plans.
+ * Errors as qlin_forward_group's argument checks.
+ */
+int qlin_group_plan(int64_t n, const qlin_t *hs, int path, int64_t split_k, int64_t M, int64_t workspace_bytes,
+                    int64_t *workspace_needed, char *buf, int64_t buflen);
+
+/* qlin_workspace_bytes -- device bytes of the handle's own workspace (0 when
+ * its plans for M <= 16 never cut the K range). */
+int qlin_workspace_bytes(qlin_t h, int64_t *bytes);
+
+/* qlin_destroy -- free the handle and its device memory.  The runtime's free
+ * waits for the device's outstanding work first, so a forward still in
+ * flight completes; captured graphs that use the handle must not be replayed
+ * afterwards.  NULL-safe. */
 void qlin_destroy(qlin_t h);
 
 /* qlin_last_error -- message of the calling thread's last failure ("" if none). */
@@ -163,8 +217,11 @@ int qlin_last_status(void);
  *
  * qlin_unpack_codes: q_out DEVICE uint8 [N][K], codes in [0, 15].
  * qlin_dequantize:   w_out DEVICE bf16 [N][K]; routine 0 = the matrix-core
- *                    routine (SKINNY/TILED paths), 1 = the vector-ALU routine
- *                    (GEMV path).  Both must give identical bits.
+ *                    routine (SKINNY/TILED/REGS paths), 1 = the vector-ALU
+ *                    routine (GEMV path).  Both must give identical bits.
+ *                    The routine argument exists because the library has two
+ *                    dequantization routes and each must be checked bit by
+ *                    bit against the definition.
  * Outputs must be 16-byte aligned.  Asynchronous on stream.
  */
 int qlin_unpack_codes(qlin_t h, uint8_t *q_out, void *stream);

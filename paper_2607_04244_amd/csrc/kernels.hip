@@ -160,14 +160,45 @@ __global__ void k_dequant_valu(const uint4 *__restrict__ codes, const void *__re
 
 // ------------------------------------------------------------------ forward
 
-// Column range and K chunk of workgroup `bid`.
-struct WgWork { int c, jn, t0, Tn, g0, Kc; };
+// Column range, member and K chunk of workgroup `bid`: chunk c, range jn
+// (over all members), the member's tiles [t0, t0 + Tn) and groups
+// [g0, g0 + Kc), and the member's weights and output.
+struct WgWork {
+    int c, jn, t0, Tn, g0, Kc;
+    const uint4 *codes;
+    const void *sz;
+    uint16_t *y;
+    int N;
+};
+// Everything here is wave-uniform scalar work at the start of the kernel:
+// the arguments arrive in one batch of scalar loads (the range starts are one
+// contiguous array, every index static, and the chunk needs no division),
+// then the member's fields in one more.
 __device__ inline WgWork wg_work(const FwdArgs &a, int bid) {
     WgWork w;
-    w.c = bid / a.Gn;                         // once per workgroup, scalar
+    // bid / Gn as a multiply-high by ceil(2^32 / Gn): exact because bid * Gn
+    // stays below 2^32 (bid < 64 * 4096 workgroups, Gn <= 4096); for Gn = 1
+    // the reciprocal is 0 and the chunk is bid itself
+    w.c = (int)(__umulhi((uint32_t)bid, a.inv_gn) + (a.Gn == 1 ? (uint32_t)bid : 0u));
     w.jn = bid - w.c * a.Gn;
-    w.t0 = w.jn * a.Nq + min(w.jn, a.Nr);
-    w.Tn = a.Nq + (w.jn < a.Nr ? 1 : 0);
+    int m = 0, g0 = 0;                        // the member owning range jn, its first range
+#pragma unroll
+    for (int i = 1; i < kMaxMembers; ++i)
+        if (w.jn >= a.gn0[i]) {
+            m = i;
+            g0 = a.gn0[i];
+        }
+    // one scalar load of the member's fields at a computed offset (reading a
+    // member at a fixed index as well would make the compiler copy the
+    // whole argument block to scratch memory)
+    const FwdMember &f = a.mem[m];
+    w.codes = f.codes;
+    w.sz = f.sz;
+    w.y = f.y;
+    w.N = f.N;
+    const int j = w.jn - g0;
+    w.t0 = j * f.Nq + min(j, f.Nr);
+    w.Tn = f.Nq + (j < f.Nr ? 1 : 0);
     w.g0 = w.c * a.Kq + min(w.c, a.Kr);
     w.Kc = a.Kq + (w.c < a.Kr ? 1 : 0);
     return w;
@@ -204,7 +235,7 @@ __device__ inline uint32_t ws_region(const FwdArgs &a, int c, int jn) {      // 
 __device__ inline void store_quarter(const FwdArgs &a, const WgWork &w, int it, int m, int n, const float s[4],
                                      bool direct) {
     if (direct) {
-        *(uint2 *)(a.y + (size_t)m * a.N + n) = make_uint2(cvt_pk_bf16(s[0], s[1]), cvt_pk_bf16(s[2], s[3]));
+        *(uint2 *)(w.y + (size_t)m * w.N + n) = make_uint2(cvt_pk_bf16(s[0], s[1]), cvt_pk_bf16(s[2], s[3]));
     } else {
         const uint32_t off = ws_region(a, w.c, w.jn) + (uint32_t)it * 16u;
         __builtin_amdgcn_raw_buffer_store_b128(
@@ -264,7 +295,7 @@ __device__ inline void reduce_chunks(const FwdArgs &a, const WgWork &w) {
         o.y = cvt_pk_bf16(s[2], s[3]);
         o.z = cvt_pk_bf16(s[4], s[5]);
         o.w = cvt_pk_bf16(s[6], s[7]);
-        *(uint4 *)(a.y + (size_t)m * a.N + n) = o;
+        *(uint4 *)(w.y + (size_t)m * w.N + n) = o;
     }
     if (tid == 0) __hip_atomic_store(&a.counters[w.jn], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -385,12 +416,10 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     //    block (its blocks span at most Tn Kb KiB, well inside the 32-bit
     //    range), so the block offset is a scalar operand of the load.
     //    Prefetches past the wave's last block (the last kDepth of the loop,
-    //    or all of them for a wave with an empty range) are never consumed:
-    //    they go through a resource of size zero, so every path still issues
-    //    the same loads (the wait counts stay static) but these return zero
-    //    without touching memory.  Re-reading a real block instead would keep
-    //    the wave waiting a full memory round trip after its last block,
-    //    since the code after the loop reuses their registers.
+    //    or all of them for a wave with an empty range) are clamped to the
+    //    wave's last block (block U - 1 of the workgroup for an empty range):
+    //    every path issues the same loads, so the wait counts stay static, and
+    //    these re-reads are never consumed.
     const bool kc1 = w.Kc == 1;
     const uint32_t inv_kc = kc1 ? 0u : 0xFFFFFFFFu / (uint32_t)w.Kc + 1u;
     const uint32_t kc1_mask = kc1 ? 0xFFFFFFFFu : 0u;       // selects u itself when Kc == 1, without a branch
@@ -401,9 +430,9 @@ __global__ void __launch_bounds__(kThreads) k_skinny(FwdArgs a) {
     constexpr int kSzBytes = SYM ? 2 : 4;
     const int span = w.Tn * a.Kb;                      // blocks from base to past the workgroup's last
     const __amdgpu_buffer_rsrc_t rcodes =
-        __builtin_amdgcn_make_buffer_rsrc((void *)(a.codes + base * 64), 0, span * 1024, kRsrcFlags);
+        __builtin_amdgcn_make_buffer_rsrc((void *)(w.codes + base * 64), 0, span * 1024, kRsrcFlags);
     const __amdgpu_buffer_rsrc_t rsz = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)((const char *)a.sz + base * kTileN * kSzBytes), 0, span * kTileN * kSzBytes, kRsrcFlags);
+        (void *)((const char *)w.sz + base * kTileN * kSzBytes), 0, span * kTileN * kSzBytes, kRsrcFlags);
     uint4 cb[kDepth];
     uint32_t sb[kDepth];
     auto fetch = [&](int d, uint32_t u) {
@@ -622,8 +651,8 @@ __global__ void __launch_bounds__(kThreads) k_mfma16(FwdArgs a) {
 #pragma unroll
             for (int t = 0; t < TN; ++t) {
                 const size_t b = base + (size_t)min(max(t, ta), tb - 1) * a.Kb;
-                B.c[t] = load_block_nt(a.codes, b * 64 + lane);
-                B.s[t] = load_sz_nt<SYM>(a.sz, b * kTileN + lm);
+                B.c[t] = load_block_nt(w.codes, b * 64 + lane);
+                B.s[t] = load_sz_nt<SYM>(w.sz, b * kTileN + lm);
             }
 #pragma unroll
             for (int j = 0; j < 4; ++j) B.x[j] = load_xfrag(a, w.g0 + kbl, j, lane);
@@ -696,13 +725,13 @@ __global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
 #pragma unroll
             for (int t = 0; t < TN; ++t) {
                 const size_t b = base + (size_t)min(max(t, ta), tb - 1) * a.Kb;
-                B.c[t] = load_block_nt(a.codes, b * 64 + lane);
+                B.c[t] = load_block_nt(w.codes, b * 64 + lane);
                 if constexpr (SYM) {
-                    const uint2 h = __builtin_bit_cast(uint2, __builtin_nontemporal_load((const v2u *)((const uint16_t *)a.sz + b * kTileN + 4 * b2)));
+                    const uint2 h = __builtin_bit_cast(uint2, __builtin_nontemporal_load((const v2u *)((const uint16_t *)w.sz + b * kTileN + 4 * b2)));
                     B.s[t] = make_uint4((h.x & 0xFFFFu) | (kZcSymmetric << 16), (h.x >> 16) | (kZcSymmetric << 16),
                                         (h.y & 0xFFFFu) | (kZcSymmetric << 16), (h.y >> 16) | (kZcSymmetric << 16));
                 } else {
-                    B.s[t] = __builtin_bit_cast(uint4, __builtin_nontemporal_load((const v4u *)((const uint32_t *)a.sz + b * kTileN + 4 * b2)));
+                    B.s[t] = __builtin_bit_cast(uint4, __builtin_nontemporal_load((const v4u *)((const uint32_t *)w.sz + b * kTileN + 4 * b2)));
                 }
             }
 #pragma unroll

@@ -36,22 +36,33 @@ enum Kern {
     kKernTiled = 3     // k_tiled: any M, 128 x 256 output blocks, x and weights staged in LDS (TILED path)
 };
 
-// Arguments of one forward launch.  The K range [0, Kb) of groups is cut into
-// S chunks and the Nt column tiles into Gn ranges; workgroup b handles chunk
-// b / Gn and column range b % Gn.  Range j holds Nq (+1 for j < Nr) tiles
-// and chunk c holds Kq (+1 for c < Kr) groups, so the kernels need no
-// division to find their work.
-struct FwdArgs {
+// Arguments of one forward launch of the decode kernels, over one linear or
+// over a group of up to kMaxMembers linears that share x (same K).  The K
+// range [0, Kb) of groups is cut into S chunks and the column tiles of the
+// members into Gn ranges in all; workgroup b handles chunk b / Gn and column
+// range b % Gn.  Ranges [gn0, gn0 + its range count) belong to one member,
+// whose Nt tiles they split as Nq (+1 for its first Nr ranges), so the
+// kernels need no division to find their work.
+constexpr int kMaxMembers = 8;
+struct FwdMember {
     const uint4 *codes;     // device layout, Nt * Kb blocks of 1 KiB
     const void *sz;         // per (tile, group, column): u32 s | zc << 16 with zc = -(128 + z), or u16 s (symmetric)
-    const uint16_t *x;      // [M][K] bf16
     uint16_t *y;            // [M][N] bf16
+    int N;                  // output columns
+    int Nq, Nr;
+};
+struct FwdArgs {
+    const uint16_t *x;      // [M][K] bf16, shared by all members
     float *ws;              // fp32 partial sums (S > 1): S * Gn regions of TnMax * M * 16
     uint32_t *counters;     // [Gn] arrival counters (S > 1), zero between launches
-    int M, K, N, Kb, Nt, S, Gn;
-    int Nq, Nr, Kq, Kr;
-    int TnMax;              // Nq + (Nr > 0): tiles of the widest column range
+    int M, K, Kb, S, Gn;
+    uint32_t inv_gn;        // ceil(2^32 / Gn) (0 for Gn = 1): chunk of workgroup b = umulhi(b, inv_gn)
+    int Kq, Kr;
+    int TnMax;              // tiles of the widest column range
     uint32_t ws_bytes;      // size of ws (bounds of its buffer descriptor)
+    int nmem;               // members, 1 .. kMaxMembers
+    int gn0[kMaxMembers];   // first column range of each member (Gn for absent members)
+    FwdMember mem[kMaxMembers];
 };
 static_assert((kWaves & (kWaves - 1)) == 0, "waves per workgroup must be a power of two");
 

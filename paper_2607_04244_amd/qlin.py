@@ -27,7 +27,8 @@ PATH_AUTO, PATH_GEMV, PATH_SKINNY, PATH_TILED, PATH_REGS = 0, 1, 2, 3, 4
 EXPORTS = ("qlin_create", "qlin_create_symmetric", "qlin_forward", "qlin_forward_path",
            "qlin_plan", "qlin_destroy", "qlin_last_error", "qlin_unpack_codes",
            "qlin_dequantize", "qlin_shape", "qlin_last_status", "qlin_stream_read", "qlin_quantize",
-           "qlin_swa_plan", "qlin_swa_attention")
+           "qlin_swa_plan", "qlin_swa_attention", "qlin_forward_group", "qlin_group_plan",
+           "qlin_workspace_bytes")
 
 _lib = None
 
@@ -76,6 +77,12 @@ def lib():
                                 ctypes.c_char_p, I64]
     L.qlin_swa_attention.restype = I32
     L.qlin_swa_attention.argtypes = [I64, I64, I64, I64, I64, I64, I64, I64, VP, VP, VP, VP, VP, I64, VP]
+    L.qlin_forward_group.restype = I32
+    L.qlin_forward_group.argtypes = [I64, VP, I32, I64, I64, VP, VP, VP, I64, VP]
+    L.qlin_group_plan.restype = I32
+    L.qlin_group_plan.argtypes = [I64, VP, I32, I64, I64, I64, ctypes.POINTER(I64), ctypes.c_char_p, I64]
+    L.qlin_workspace_bytes.restype = I32
+    L.qlin_workspace_bytes.argtypes = [P, ctypes.POINTER(I64)]
     L.qlin_shape.restype = I32
     L.qlin_shape.argtypes = [P, ctypes.POINTER(I64), ctypes.POINTER(I64)]
     _lib = L
@@ -165,6 +172,32 @@ def qlin_plan(h, path, split_k, M):
     return buf.value.decode()
 
 
+def _handles(hs):
+    arr = (ctypes.c_void_p * len(hs))(*hs)
+    return arr
+
+
+def qlin_forward_group(hs, path, split_k, M, x_ptr, y_ptrs, ws_ptr, ws_bytes, stream):
+    """hs: sequence of handles; y_ptrs: sequence of device addresses."""
+    ys = (ctypes.c_void_p * len(y_ptrs))(*y_ptrs)
+    return lib().qlin_forward_group(len(hs), _handles(hs), path, split_k, M, x_ptr, ys, ws_ptr, ws_bytes, stream)
+
+
+def qlin_group_plan(hs, path, split_k, M, ws_bytes=-1):
+    """(workspace bytes the plan uses, plan text) for a workspace of ws_bytes (-1: no limit)."""
+    need = ctypes.c_int64()
+    buf = ctypes.create_string_buffer(256)
+    _check(lib().qlin_group_plan(len(hs), _handles(hs), path, split_k, M, ws_bytes, ctypes.byref(need), buf,
+                                 len(buf)))
+    return need.value, buf.value.decode()
+
+
+def qlin_workspace_bytes(h):
+    b = ctypes.c_int64()
+    _check(lib().qlin_workspace_bytes(h, ctypes.byref(b)))
+    return b.value
+
+
 def qlin_destroy(h):
     lib().qlin_destroy(h)
 
@@ -220,10 +253,13 @@ def swa_attention(q, k, v, window, T=None, splits=0, out=None, workspace=None):
     Hkv, cap, _ = k.shape
     if v.shape != k.shape:
         raise ValueError("k and v must have the same shape")
+    if k.device != q.device or v.device != q.device:
+        raise ValueError("q, k and v must be on one device")
     T = cap if T is None else T
     S, ws_bytes, _ = qlin_swa_plan(Hq, Hkv, D, nq, T, window, splits)
     if out is None:
         out = torch.empty((Hq, nq, D), dtype=torch.bfloat16, device=q.device)
+    _check_out(out, (Hq, nq, D), q.device)
     if ws_bytes and workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=q.device)
     ws_ptr = workspace.data_ptr() if workspace is not None else None
@@ -231,6 +267,45 @@ def swa_attention(q, k, v, window, T=None, splits=0, out=None, workspace=None):
     _check(qlin_swa_attention(Hq, Hkv, D, nq, T, cap, window, splits, q.data_ptr(), k.data_ptr(), v.data_ptr(),
                               out.data_ptr(), ws_ptr, ws_len, torch.cuda.current_stream().cuda_stream))
     return out
+
+
+def _check_out(out, shape, device):
+    import torch
+    if (not isinstance(out, torch.Tensor) or out.dtype != torch.bfloat16 or out.device != device
+            or tuple(out.shape) != tuple(shape) or not out.is_contiguous()):
+        raise ValueError(f"out must be a contiguous bf16 tensor of shape {tuple(shape)} on {device}")
+
+
+def new_workspace(nbytes, device=None):
+    """A zero-filled device workspace for forward_group (zero before first use)."""
+    import torch
+    return torch.zeros(max(int(nbytes), 16), dtype=torch.uint8, device=device or "cuda")
+
+
+def forward_group(lins, x, outs=None, path=PATH_AUTO, split_k=0, workspace=None):
+    """One launch over QLinear layers that share x (qlin_forward_group).
+    ``workspace``: a zero-filled CUDA uint8 tensor (new_workspace), or None
+    for plans without a K split.  Returns the list of outputs."""
+    import torch
+    K = lins[0].K
+    for l in lins:
+        if l.K != K:
+            raise ValueError("the layers of a group must share K")
+    x = lins[0]._check_x(x)
+    M = x.shape[0]
+    if outs is None:
+        outs = [torch.empty((M, l.N), dtype=torch.bfloat16, device=x.device) for l in lins]
+    for l, o in zip(lins, outs):
+        _check_out(o, (M, l.N), x.device)
+    wp, wb = (workspace.data_ptr(), workspace.numel() * workspace.element_size()) if workspace is not None else (None, 0)
+    _check(qlin_forward_group([l.h for l in lins], path, split_k, M, x.data_ptr(), [o.data_ptr() for o in outs],
+                              wp, wb, torch.cuda.current_stream().cuda_stream))
+    return outs
+
+
+def group_plan(lins, M, path=PATH_AUTO, split_k=0, ws_bytes=-1):
+    """(workspace bytes, plan text) of forward_group over lins for M rows."""
+    return qlin_group_plan([l.h for l in lins], path, split_k, M, ws_bytes)
 
 
 class QLinear:
@@ -246,6 +321,8 @@ class QLinear:
             packed = np.asarray(packed)
         self.N, K8 = packed.shape
         self.K = K8 * 8
+        import torch
+        self.device = torch.device("cuda", torch.cuda.current_device())
         if zeros is None:
             self.h = qlin_create_symmetric(self.K, self.N, group, packed, scales)
         else:
@@ -255,17 +332,30 @@ class QLinear:
         import torch
         return torch.cuda.current_stream().cuda_stream
 
-    def forward(self, x, out=None, path=PATH_AUTO, split_k=0):
+    def _check_x(self, x):
         import torch
-        if x.dtype != torch.bfloat16 or not x.is_cuda or x.dim() != 2 or x.shape[1] != self.K:
-            raise ValueError("x must be a CUDA bf16 tensor of shape [M, K]")
-        x = x.contiguous()
+        if x.dtype != torch.bfloat16 or x.device != self.device or x.dim() != 2 or x.shape[1] != self.K:
+            raise ValueError(f"x must be a bf16 tensor of shape [M, {self.K}] on {self.device}")
+        return x.contiguous()
+
+    def forward(self, x, out=None, path=PATH_AUTO, split_k=0, workspace=None):
+        """y = x . w^T.  With ``workspace`` (new_workspace) the call goes
+        through qlin_forward_group and may use the plans that need it."""
+        import torch
+        if workspace is not None:
+            return forward_group([self], x, None if out is None else [out], path, split_k, workspace)[0]
+        x = self._check_x(x)
         M = x.shape[0]
         y = out if out is not None else torch.empty((M, self.N), dtype=torch.bfloat16, device=x.device)
+        _check_out(y, (M, self.N), x.device)
         _check(qlin_forward_path(self.h, path, split_k, M, x.data_ptr(), y.data_ptr(), self._stream()))
         return y
 
     __call__ = forward
+
+    def workspace_bytes(self):
+        """Bytes of the handle's own workspace."""
+        return qlin_workspace_bytes(self.h)
 
     def plan(self, M, path=PATH_AUTO, split_k=0):
         return qlin_plan(self.h, path, split_k, M)

@@ -111,6 +111,32 @@ def model_linear(layer, proj):
     return dict(name=name, K=K, N=N, packed=packed, scales=scales, zeros=zeros)
 
 
+# The drafter (Sec. 3.2: five layers, hidden size 2560, block size 16, about
+# 537M parameters; Sec. 3.3: group-wise symmetric INT4, group 128).  Its
+# layers have the decoder shapes above; the context projection maps the
+# hidden states of five target layers (5 x 2560) to 2560, which with the
+# five layers (504.6M) accounts for the stated parameter count (537.4M).
+DRAFTER_LAYERS = 5
+DRAFTER_FC = ("fc", 5 * 2560, 2560)
+
+
+def drafter_linear_seed(layer, proj):
+    """Seed of drafter linear ``proj`` (index into LAYER_SHAPES, or
+    len(LAYER_SHAPES) for the context projection, which has no layer)."""
+    return 5_000_000 + (100 if proj == len(LAYER_SHAPES) else 10 * layer + proj)
+
+
+def drafter_linear(layer, proj):
+    """Weights of one drafter linear in the symmetric format: packed codes and
+    scales only (the zero-point is 8).  Draw order: packed words, scales."""
+    name, K, N = DRAFTER_FC if proj == len(LAYER_SHAPES) else LAYER_SHAPES[proj]
+    rng = np.random.default_rng(drafter_linear_seed(layer, proj))
+    packed = rng.integers(0, 2 ** 32, size=(N, K // GROUP * 16), dtype=np.uint32)
+    lo, hi = CONFIGS[3]["s_range"]
+    scales = f32_to_bf16_bits(rng.uniform(lo, hi, size=(N, K // GROUP)).astype(np.float32))
+    return dict(name=name, K=K, N=N, packed=packed, scales=scales)
+
+
 def model_activations(cfg_id, M, K):
     """Activations for the whole-model workloads: one x per (M, K)."""
     c = CONFIGS[cfg_id]

@@ -228,3 +228,20 @@ def test_attention_rejects_bad_arguments():
     assert call(o=w + 4096) == qlin.QLIN_ERR_INVALID                 # out overlaps the workspace
     assert call(D=96) == qlin.QLIN_ERR_UNSUPPORTED
     assert qlin.qlin_last_status() == qlin.QLIN_ERR_UNSUPPORTED
+
+
+def test_group_calls_reject_bad_arguments_without_a_device():
+    """Checks of the grouped launch that need no handle (no HIP call)."""
+    L = qlin.lib()
+    A = 1 << 32
+    assert L.qlin_forward_group(0, None, 0, 0, 16, A, None, None, 0, None) == qlin.QLIN_ERR_INVALID
+    assert L.qlin_forward_group(1, None, 0, 0, 16, A, None, None, 0, None) == qlin.QLIN_ERR_INVALID
+    assert L.qlin_forward_group(9, None, 0, 0, 16, A, None, None, 0, None) == qlin.QLIN_ERR_INVALID
+    hs = (qlin.ctypes.c_void_p * 2)(None, None)
+    assert L.qlin_forward_group(2, hs, 0, 0, 16, A, None, None, 0, None) == qlin.QLIN_ERR_INVALID
+    assert "NULL handle" in qlin.last_error()
+    assert L.qlin_forward_group(1, hs, 0, 0, 16, A, None, A, -5, None) == qlin.QLIN_ERR_INVALID
+    assert L.qlin_forward_group(1, hs, 0, 0, 16, A, None, None, 64, None) == qlin.QLIN_ERR_INVALID
+    need = qlin.ctypes.c_int64()
+    assert L.qlin_group_plan(0, None, 0, 0, 16, -1, qlin.ctypes.byref(need), None, 0) == qlin.QLIN_ERR_INVALID
+    assert L.qlin_workspace_bytes(None, qlin.ctypes.byref(need)) == qlin.QLIN_ERR_INVALID

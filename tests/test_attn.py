@@ -131,6 +131,58 @@ def test_window_of_one_returns_the_own_value_row_exactly():
         assert np.array_equal(out[hq], v[hq // 4, T - nq:T]), hq
 
 
+@pytest.mark.parametrize("Hq,Hkv,T,W,splits", [
+    (8, 2, 600, 7, 0),          # half window 3: both edges inside the cache for most queries
+    (8, 2, 600, 8, 1),          # even window, one key range
+    (8, 2, 600, 9, 3),          # odd window, key ranges cut inside the window
+    (8, 2, 2000, 41, 0),        # half window 20: right edges beyond the cache
+    (8, 2, 2000, 40, 5),
+    (32, 8, 8192, 1024, 0),     # the benchmarked swa1024 shape and plan
+    (32, 8, 8192, 1025, 4),
+    (32, 8, 8192, 2048, 0),     # swa2048
+    (32, 8, 8192, 2049, 17),
+])
+def test_window_edge_is_exact(Hq, Hkv, T, W, splits):
+    """The window edge, exactly.  With q = 0 every visible key gets weight 1
+    (exp of 0, exact in bf16), so out = (sum of visible value rows) / n.
+    Value rows are zero except markers: for block query i at position p,
+    dimension 4 i + r holds 1 at key p - h - 1, p - h, p + h, p + h + 1
+    (r = 0..3, h = W / 2, keys outside the cache skipped).  A key admitted
+    or dropped at the edge changes a dimension from 0 to 1/n or back, so
+    every dimension whose visible sum is 0 must come out as an exact zero,
+    and every other within the rounding of 1/n's multiples."""
+    nq = 16
+    h = W // 2
+    rng = np.random.default_rng(T + W)
+    k = gen.draw_attention(rng, 1, Hkv, 1, T, 1.0)[1]
+    q = np.zeros((Hq, nq, D), np.uint16)
+    v = np.zeros((Hkv, T, D), np.uint16)
+    for i in range(nq):
+        p = T - nq + i
+        for role, j in enumerate((p - h - 1, p - h, p + h, p + h + 1)):
+            if 0 <= j < T:
+                v[:, j, 4 * i + role] = 0x3F80
+    out = host_f64(run(q, k, v, T, W, splits))
+    vis = ar.visible(T, W, nq).astype(np.float64)
+    vf = ar.bf16_to_f64(v)
+    G = Hq // Hkv
+    for hq in range(Hq):
+        want = (vis @ vf[hq // G]) / vis.sum(axis=1, keepdims=True)      # [nq][D]
+        got = out[hq]
+        zero = want == 0
+        assert np.all(got[zero] == 0), f"head {hq}: {np.argwhere((got != 0) & zero)[:5]} should be 0"
+        assert np.all(np.abs(got[~zero] - want[~zero]) <= 2.0 ** -8 * want[~zero]), f"head {hq}"
+        # each query's own markers: the two just outside the window are
+        # exact zeros, the two on its edge are not
+        for i in range(nq):
+            p = T - nq + i
+            assert got[i, 4 * i] == 0 and got[i, 4 * i + 3] == 0, (hq, i)
+            if p - h >= 0:
+                assert got[i, 4 * i + 1] > 0, (hq, i)
+            if p + h < T:
+                assert got[i, 4 * i + 2] > 0, (hq, i)
+
+
 def test_zero_queries_average_the_visible_values():
     """q = 0: uniform weights, the output is the mean of the visible rows."""
     T, W = 600, 128

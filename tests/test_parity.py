@@ -37,7 +37,15 @@ def make(c, symmetric=False):
 
 
 def run(lin, x_bits, path=AUTO, split_k=0):
-    y = lin.forward(dev(x_bits), path=path, split_k=split_k)
+    """One forward.  A forced path or split runs with a caller workspace of
+    the size its unconstrained plan reports (qlin_group_plan); the automatic
+    plan runs through qlin_forward_path with the handle's own workspace."""
+    x = dev(x_bits)
+    if split_k > 0 or path != AUTO:
+        need, _ = qlin.group_plan([lin], x.shape[0], path, split_k)
+        y = lin.forward(x, path=path, split_k=split_k, workspace=qlin.new_workspace(need))
+    else:
+        y = lin.forward(x, path=path, split_k=split_k)
     torch.cuda.synchronize()
     return host_bits(y)
 
@@ -215,7 +223,7 @@ def test_tiled_block_shapes_match_oracle(M, K, N, shape):
     every output compared."""
     c = gen.random_case(M + K + N, M, K, N, sigma=1.0)
     lin = make(c)
-    assert f"kernel={shape}" in lin.plan(M, TILED)
+    assert f"kernel={shape}" in qlin.group_plan([lin], M, TILED)[1]
     assert_close(run(lin, c["x"], TILED), oracle(c), f"{shape} M={M} K={K} N={N}")
     lin.close()
 
@@ -229,7 +237,7 @@ def test_tiled_split_k_matches_oracle(M, K, N, split):
     counters were left at zero."""
     c = gen.random_case(7 * M + K + N + split, M, K, N, sigma=1.0)
     lin = make(c)
-    assert f"split={split} " in lin.plan(M, TILED, split)
+    assert f"split={split} " in qlin.group_plan([lin], M, TILED, split)[1]
     y_ref = oracle(c)
     assert_close(run(lin, c["x"], TILED, split), y_ref, f"tiled M={M} K={K} N={N} S={split}")
     assert_close(run(lin, c["x"], TILED, split), y_ref, f"tiled M={M} K={K} N={N} S={split}, second call")
@@ -247,9 +255,14 @@ def test_prefill_narrow_layers_take_the_split_tiled_kernel(K, N):
     M = 128
     c = gen.random_case(K + 5, M, K, N, sigma=1.0)
     lin = make(c)
-    plan = lin.plan(M)
-    assert "kernel=k_tiled<4,2>" in plan and "split=1 " not in plan, plan
-    assert_close(run(lin, c["x"]), oracle(c), f"M={M} K={K} N={N}")
+    need, plan = qlin.group_plan([lin], M)
+    assert "kernel=k_tiled<4,2>" in plan and "split=1 " not in plan and need > 0, plan
+    y_ref = oracle(c)
+    y = lin.forward(dev(c["x"]), workspace=qlin.new_workspace(need))
+    torch.cuda.synchronize()
+    assert_close(host_bits(y), y_ref, f"M={M} K={K} N={N} with a caller workspace")
+    # the handle's own workspace (sized for M <= 16) runs a plan that fits it
+    assert_close(run(lin, c["x"]), y_ref, f"M={M} K={K} N={N} own workspace: {lin.plan(M)}")
     lin.close()
 
 
