@@ -193,6 +193,24 @@ int qlin_forward_group(int64_t n, const qlin_t *hs, int path, int64_t split_k, i
 int qlin_group_plan(int64_t n, const qlin_t *hs, int path, int64_t split_k, int64_t M, int64_t workspace_bytes,
                     int64_t *workspace_needed, char *buf, int64_t buflen);
 
+/*
+ * qlin_forward_group_noalloc -- qlin_forward_group without a workspace
+ * argument and without any allocation, for callers that cannot allocate
+ * device memory (code under HIP-graph capture, tight serving loops, hosts
+ * that forbid allocation).  The K-split scratch comes from a static array of
+ * the library on each device (16 MiB, held from the first handle created on
+ * the device until the process ends); its arrival counters are cleared once
+ * when that first handle is created, and every call leaves them at zero.
+ *
+ * Arguments and plan as qlin_forward_group with an unlimited workspace.  All
+ * calls on one device share the array: calls that overlap in time on one
+ * device (different streams, or threads) race and must not be issued.
+ * Errors as qlin_forward_group, plus UNSUPPORTED when that plan needs more
+ * scratch than the array holds (qlin_group_plan reports the need).
+ */
+int qlin_forward_group_noalloc(int64_t n, const qlin_t *hs, int path, int64_t split_k, int64_t M,
+                               const uint16_t *x, uint16_t *const *ys, void *stream);
+
 /* qlin_workspace_bytes -- device bytes of the handle's own workspace (0 when
  * its plans for M <= 16 never cut the K range). */
 int qlin_workspace_bytes(qlin_t h, int64_t *bytes);

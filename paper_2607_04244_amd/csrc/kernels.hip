@@ -34,6 +34,7 @@
 
 #include <algorithm>
 #include <cstdio>
+#include <mutex>
 
 namespace qlin {
 
@@ -865,6 +866,41 @@ __global__ void __launch_bounds__(512) k_stream_read(const uint4 *__restrict__ p
 hipError_t launch_stream_read(const void *buf, size_t bytes, int grid, uint32_t *sink, hipStream_t st) {
     hipLaunchKernelGGL(k_stream_read, dim3(grid), dim3(512), 0, st, (const uint4 *)buf, bytes / 16, sink);
     return hipGetLastError();
+}
+
+// ------------------------------------------------------------------ static scratch
+
+// The split-K scratch of qlin_forward_group_noalloc: arrival counters and
+// partial sums in the layout of any workspace, in a file-scope device array
+// that each device holds from the library's load until the process ends.
+// Host code never passes `scratch` itself to a kernel (in host code the name
+// stands for a host-side shadow, not a device address): it uses the address
+// hipGetSymbolAddress returns for the current device.
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t static_scratch_setup(int device, hipStream_t st) {
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[device]) return hipSuccess;
+    void *ptr = nullptr;
+    hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    // the arrival counters must start at zero (every launch leaves them so)
+    if ((e = hipMemsetAsync(ptr, 0, kScratchCounterBytes, st)) != hipSuccess) return e;
+    if ((e = hipStreamSynchronize(st)) != hipSuccess) return e;
+    g_scratch_ptr[device] = ptr;
+    return hipSuccess;
+}
+
+void *static_scratch(int device) {
+    if (device < 0 || device >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    return g_scratch_ptr[device];
 }
 
 // ------------------------------------------------------------------ host launchers

@@ -79,6 +79,7 @@ constexpr size_t kMaxWsBytes = 0xFFFFFF00u;   // buffer-descriptor range of the 
 // and handles can share one workspace in stream order.
 constexpr int kMaxCounters = 4096;
 constexpr size_t kCounterBytes = (size_t)kMaxCounters * 4;
+static_assert(kCounterBytes == kScratchCounterBytes, "the static scratch has the workspace layout");
 
 // Test hook: QLIN_FAULT=alloc makes every device allocation of this library fail.
 hipError_t dev_alloc(void **p, size_t bytes) {
@@ -828,6 +829,8 @@ qlin_t create_impl(int64_t K, int64_t N, int64_t group, const uint32_t *packed, 
         return bail("copy zeros", e);
     if (h->ws_bytes && (e = hipMemsetAsync(h->ws, 0, h->ws_bytes, st)) != hipSuccess)
         return bail("clear workspace", e);
+    // set-up of this device's static scratch (qlin_forward_group_noalloc), once
+    if ((e = static_scratch_setup(h->device, st)) != hipSuccess) return bail("static scratch set-up", e);
     if ((e = launch_repack((const uint32_t *)canon, (const uint16_t *)sc, (const uint16_t *)zc, h->codes, h->sz,
                            (int)K, (int)N, symmetric, st)) != hipSuccess)
         return bail("repack launch", e);
@@ -984,6 +987,29 @@ int qlin_forward_group(int64_t n, const qlin_t *hs, int path, int64_t split_k, i
     if (rc != QLIN_OK || M == 0) return rc;
     const hipStream_t st = (hipStream_t)stream;
     return launch_all(t, path, split_k, M, x, ys, workspace, (size_t)workspace_bytes, st);
+}
+
+int qlin_forward_group_noalloc(int64_t n, const qlin_t *hs, int path, int64_t split_k, int64_t M,
+                               const uint16_t *x, uint16_t *const *ys, void *stream) {
+    clear_err();
+    Target t;
+    if (group_target_ws(n, hs, -1, &t) != QLIN_OK) return last_status();
+    if (!ys) return fail(QLIN_ERR_INVALID, "NULL output array");
+    if (split_k < 0 || split_k > t.Kb) return fail(QLIN_ERR_INVALID, "split_k must be in [0, K/128]");
+    if (check_path_rows(path, M) != QLIN_OK) return last_status();
+    void *ws = static_scratch(t.mem[0]->device);
+    if (!ws) return fail(QLIN_ERR_INVALID, "no static scratch on device %d", t.mem[0]->device);
+    int rc = check_launch(t, M, x, ys, ws, kStaticScratchBytes);
+    if (rc != QLIN_OK || M == 0) return rc;
+    // the plan qlin_forward_group runs with a workspace of unlimited size,
+    // refused when its scratch exceeds the static array
+    size_t need = 0;
+    if ((rc = workspace_need(t, path, split_k, M, &need)) != QLIN_OK) return rc;
+    if (need > kStaticScratchBytes)
+        return fail(QLIN_ERR_UNSUPPORTED, "this plan needs %zu bytes of scratch, the static array holds %zu "
+                    "(use qlin_forward_group with a workspace)", need, kStaticScratchBytes);
+    set_capacity(t, kStaticScratchBytes);
+    return launch_all(t, path, split_k, M, x, ys, ws, kStaticScratchBytes, (hipStream_t)stream);
 }
 
 int qlin_group_plan(int64_t n, const qlin_t *hs, int path, int64_t split_k, int64_t M, int64_t workspace_bytes,

@@ -133,6 +133,17 @@ hipError_t launch_tiled(bool symmetric, TiledShape shape, const TiledArgs &a, in
 hipError_t launch_stream_read(const void *buf, size_t bytes, int grid, uint32_t *sink, hipStream_t st);
 const char *kernel_name(int kern, int mrows, int tn, bool symmetric);
 
+// Static split-K scratch (kernels.hip) for callers that cannot allocate:
+// kStaticScratchBytes per device, laid out as every workspace (counters,
+// then partials).  static_scratch_setup looks up the array's device address
+// on `device` (which must be current) once and clears its counters on st;
+// static_scratch returns that address (NULL before the set-up).
+constexpr size_t kStaticScratchBytes = (size_t)16 << 20;
+constexpr size_t kScratchCounterBytes = (size_t)16 << 10;   // the counter region of every workspace
+constexpr int kMaxDevices = 64;
+hipError_t static_scratch_setup(int device, hipStream_t st);
+void *static_scratch(int device);
+
 // ---- error state shared by the C-ABI sources (defined in qlin.cpp)
 int fail(int code, const char *fmt, ...);
 int hip_fail(hipError_t e, const char *what);

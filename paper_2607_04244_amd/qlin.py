@@ -28,7 +28,7 @@ EXPORTS = ("qlin_create", "qlin_create_symmetric", "qlin_forward", "qlin_forward
            "qlin_plan", "qlin_destroy", "qlin_last_error", "qlin_unpack_codes",
            "qlin_dequantize", "qlin_shape", "qlin_last_status", "qlin_stream_read", "qlin_quantize",
            "qlin_swa_plan", "qlin_swa_attention", "qlin_forward_group", "qlin_group_plan",
-           "qlin_workspace_bytes")
+           "qlin_workspace_bytes", "qlin_forward_group_noalloc")
 
 _lib = None
 
@@ -79,6 +79,8 @@ def lib():
     L.qlin_swa_attention.argtypes = [I64, I64, I64, I64, I64, I64, I64, I64, VP, VP, VP, VP, VP, I64, VP]
     L.qlin_forward_group.restype = I32
     L.qlin_forward_group.argtypes = [I64, VP, I32, I64, I64, VP, VP, VP, I64, VP]
+    L.qlin_forward_group_noalloc.restype = I32
+    L.qlin_forward_group_noalloc.argtypes = [I64, VP, I32, I64, I64, VP, VP, VP]
     L.qlin_group_plan.restype = I32
     L.qlin_group_plan.argtypes = [I64, VP, I32, I64, I64, I64, ctypes.POINTER(I64), ctypes.c_char_p, I64]
     L.qlin_workspace_bytes.restype = I32
@@ -181,6 +183,11 @@ def qlin_forward_group(hs, path, split_k, M, x_ptr, y_ptrs, ws_ptr, ws_bytes, st
     """hs: sequence of handles; y_ptrs: sequence of device addresses."""
     ys = (ctypes.c_void_p * len(y_ptrs))(*y_ptrs)
     return lib().qlin_forward_group(len(hs), _handles(hs), path, split_k, M, x_ptr, ys, ws_ptr, ws_bytes, stream)
+
+
+def qlin_forward_group_noalloc(hs, path, split_k, M, x_ptr, y_ptrs, stream):
+    ys = (ctypes.c_void_p * len(y_ptrs))(*y_ptrs)
+    return lib().qlin_forward_group_noalloc(len(hs), _handles(hs), path, split_k, M, x_ptr, ys, stream)
 
 
 def qlin_group_plan(hs, path, split_k, M, ws_bytes=-1):
