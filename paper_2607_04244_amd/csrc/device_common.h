@@ -217,6 +217,24 @@ __device__ inline void load_lds_x4(const void *src, const void *lds_dst) {
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, off" :: "s"(m0), "v"(src) : "memory", "m0");
 }
 
+// LDS byte address of p (wave-uniform), as a scalar.
+__device__ inline uint32_t lds_addr(const void *p) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)p);
+}
+
+// Direct-to-LDS buffer loads: lane l's 16 (4) bytes at byte offset
+// voff + soff of the resource land at LDS byte address lds + 16 l (4 l).
+// Inline assembly for the same reason as load_lds_x16; lds and soff are
+// scalars, so a load whose per-lane offset is fixed costs no vector work.
+__device__ inline void load_lds_buf16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :: "s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
+}
+__device__ inline void load_lds_buf4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, %3 offen lds"
+                 :: "s"(lds), "v"(voff), "s"(r), "s"(soff) : "memory", "m0");
+}
+
 // Barrier for LDS hand-off only.  __syncthreads() also waits for every
 // outstanding global load, which would drain the weight prefetch.
 __device__ inline void lds_barrier() {

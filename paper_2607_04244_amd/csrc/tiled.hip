@@ -84,43 +84,59 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     const int lm = lane & 15, lg = lane >> 4;
     const DiagSel dsel(lane);
 
+    // All global reads are direct-to-LDS buffer loads issued through inline
+    // assembly (load_lds_buf16 / load_lds_buf4): the compiler does not track
+    // them, so the only waits are the explicit vmcnt below and the pipeline
+    // keeps kTiledStages - 1 groups in flight across the barriers.  Each
+    // load's per-lane offset is fixed for the whole K walk and the group
+    // enters as a scalar offset, so issuing a load costs no vector
+    // instruction; the LDS destinations are scalars too.
+    //
     // x: load i of wave w fills rows kRowsPerWave w + 4 i + (lane >> 4), slot
     // position lane & 15, which holds chunk (lane & 15) ^ (row & 15) of that
-    // row.  Element offsets from x at group 0; the planner keeps M * K below 2^31.
-    uint32_t xo[kXLoads];
+    // row.  Byte offsets from x at group 0; the planner keeps M * K below
+    // 2^31, so x spans less than 4 GiB.
+    const __amdgpu_buffer_rsrc_t rx =
+        __builtin_amdgcn_make_buffer_rsrc((void *)a.x, 0, (int)((uint32_t)a.M * (uint32_t)a.K * 2u), kRsrcFlags);
+    uint32_t xv[kXLoads];
 #pragma unroll
     for (int i = 0; i < kXLoads; ++i) {
         const int r = wave * kRowsPerWave + 4 * i + lg;
         const int row = min(im * BM + r, a.M - 1);
-        xo[i] = (uint32_t)row * (uint32_t)a.K + (uint32_t)(((lane & 15) ^ (r & 15)) * 8);
+        xv[i] = ((uint32_t)row * (uint32_t)a.K + (uint32_t)(((lane & 15) ^ (r & 15)) * 8)) * 2u;
     }
-    // All global reads are direct-to-LDS loads issued through inline assembly
-    // (load_lds_x16 / load_lds_x4): the compiler does not track them, so the
-    // only waits are the explicit vmcnt below and the pipeline keeps
-    // kTiledStages - 1 groups in flight across the barriers.
+    constexpr uint32_t kXStage = BM * 16 * 16, kXLoad = 4 * 16 * 16;   // LDS bytes per stage, per load
+    const uint32_t lds_x = lds_addr(&xs[0][wave * kRowsPerWave * 16]);
     auto load_x = [&](int kb, int buf) {
 #pragma unroll
         for (int i = 0; i < kXLoads; ++i)
-            load_lds_x16(a.x + xo[i] + (uint32_t)kb * kGroup, &xs[buf][(wave * kRowsPerWave + 4 * i) * 16]);
+            load_lds_buf16(rx, xv[i], (uint32_t)kb * (kGroup * 2), lds_x + (uint32_t)buf * kXStage + i * kXLoad);
     };
     // weights: wave w loads its own tiles NW w + u (clamped to the last
-    // tile); wo = uint4 index of block (tile, 0) / 64
-    uint32_t wo[NW];
+    // tile), through resources based at the workgroup's first tile (its
+    // blocks span at most 16 Kb KiB); wv / sv = byte offsets of this lane's
+    // part of block (tile, 0)
+    const int t0 = jn * kTiles, ntw = min(kTiles, a.Nt - t0);
+    constexpr uint32_t kSzBlk = SYM ? kTileN * 2 : kTileN * 4;          // s|z bytes per block
+    const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(a.codes + (size_t)t0 * a.Kb * 64), 0, ntw * a.Kb * 1024, kRsrcFlags);
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)((const char *)a.sz + (size_t)t0 * a.Kb * kSzBlk), 0, ntw * a.Kb * (int)kSzBlk, kRsrcFlags);
+    uint32_t wv[NW], sv[NW];
 #pragma unroll
-    for (int u = 0; u < NW; ++u) wo[u] = (uint32_t)min(jn * kTiles + wave * NW + u, a.Nt - 1) * (uint32_t)a.Kb;
+    for (int u = 0; u < NW; ++u) {
+        const uint32_t tr = (uint32_t)(min(t0 + wave * NW + u, a.Nt - 1) - t0) * (uint32_t)a.Kb;   // block (tile, 0)
+        wv[u] = tr * 1024u + lane * 16u;
+        // 2-byte scales: one dword per lane covers columns 2i, 2i + 1 (read_w picks the half)
+        sv[u] = tr * kSzBlk + (SYM ? (lane & 7) : lm) * 4u;
+    }
+    constexpr uint32_t kWStage = kTiles * 64 * 16, kSStage = kTiles * 64 * 4;
+    const uint32_t lds_w = lds_addr(&ws_codes[0][wave * NW * 64]), lds_s = lds_addr(&ws_sz[0][wave * NW * 64]);
     auto load_w = [&](int kb, int buf) {
 #pragma unroll
         for (int u = 0; u < NW; ++u) {
-            const uint32_t b = wo[u] + (uint32_t)kb;
-            const int slot = (wave * NW + u) * 64;
-            load_lds_x16(a.codes + (size_t)b * 64 + lane, &ws_codes[buf][slot]);
-            if constexpr (SYM) {
-                // 2-byte scales: one dword per lane covers columns 2i, 2i + 1;
-                // read_w picks the half
-                load_lds_x4((const uint32_t *)a.sz + (size_t)b * (kTileN / 2) + (lane & 7), &ws_sz[buf][slot]);
-            } else {
-                load_lds_x4((const uint32_t *)a.sz + (size_t)b * kTileN + lm, &ws_sz[buf][slot]);
-            }
+            load_lds_buf16(rc, wv[u], (uint32_t)kb * 1024u, lds_w + (uint32_t)buf * kWStage + u * 1024u);
+            load_lds_buf4(rs, sv[u], (uint32_t)kb * kSzBlk, lds_s + (uint32_t)buf * kSStage + u * 256u);
         }
     };
     // this lane's code words and s|z word of the wave's tile t from LDS
@@ -174,11 +190,14 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
 
     // Pipeline of kTiledStages LDS buffers: groups kb + 1 .. kb + S - 1 are
     // in flight (straight into LDS) while group kb is computed.  Each step
-    // issues one group's loads (kIssued memory instructions per wave; past
-    // the last group they reload it into a buffer nobody reads), waits for
-    // group kb's, and computes it.
+    // waits for group kb's loads (kIssued memory instructions per wave), then
+    // one barrier both publishes group kb and shows that every wave is done
+    // with the previous step's buffer, which the step refills with group
+    // kb + S - 1 (past the last group the loads reload it into a buffer
+    // nobody reads) before computing group kb.
     constexpr int kIssued = kXLoads + 2 * NW;
     constexpr int S = kTiledStages;
+    static_assert(S >= 2, "the pipeline needs two stages");
 #pragma unroll
     for (int i = 0; i < S - 1; ++i) {
         load_x(min(g0 + i, g1), i);
@@ -186,13 +205,12 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     }
     int buf = 0;
     for (int kb = g0; kb <= g1; ++kb) {
+        asm volatile("s_waitcnt vmcnt(%0)" :: "n"((S - 2) * kIssued) : "memory");
+        lds_barrier();                        // group kb is in LDS for every wave; buffer nb is free
         const int nb = buf == 0 ? S - 1 : buf - 1;             // (kb - g0 + S - 1) % S
         load_x(min(kb + S - 1, g1), nb);
         load_w(min(kb + S - 1, g1), nb);
-        asm volatile("s_waitcnt vmcnt(%0)" :: "n"((S - 1) * kIssued) : "memory");
-        lds_barrier();                        // group kb is in LDS for every wave
         compute(buf);
-        lds_barrier();                        // everyone is done reading buf before it is refilled
         buf = buf == S - 1 ? 0 : buf + 1;
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the reloads past the end
