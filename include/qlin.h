@@ -155,9 +155,9 @@ int qlin_plan(qlin_t h, int path, int64_t split_k, int64_t M, char *buf, int64_t
  * that share the input x: one launch of the decode kernels covers all of
  * them (M <= 64), e.g. the q, k and v projections of a decoder layer, which
  * the target runs on every verification step (Sec. 2.2) and the drafter on
- * every drafting step (Sec. 2.3).  For M > 64 (or path TILED) the members run
- * as consecutive tiled launches.  n = 1 is a forward of one handle with a
- * caller workspace.
+ * every drafting step (Sec. 2.3).  For M > 64 (or path TILED) one tiled
+ * launch covers all members as well.  n = 1 is a forward of one handle with
+ * a caller workspace.
  *
  *   n          1 <= n <= 8 handles, all with the same K, the same format
  *              (zero-points or symmetric) and on the current device

@@ -348,7 +348,15 @@ const TunedPlan *tuned_plan(const Target &t, int M) {
     return nullptr;
 }
 
-// TILED plan for one linear: one launch over all M rows.  The block shape
+// Column blocks of a tiled launch with blocks of 4 nt tiles: each member's
+// tiles are cut on their own.
+int64_t tiled_col_blocks(const Target &t, int nt) {
+    int64_t g = 0;
+    for (int i = 0; i < t.nmem; ++i) g += (t.mem[i]->Nt + 4 * nt - 1) / (4 * nt);
+    return g;
+}
+
+// TILED plan: one launch over all M rows and all members.  The block shape
 // minimises (blocks per compute unit, rounded up) x (time of one block), with
 // the block times measured on MI355X relative to the 128 x 256 shape (same
 // K): 96 x 256 0.95, 64 x 128 0.42.  Ranked this way the three shapes come
@@ -366,7 +374,7 @@ int make_tiled_plan(const Target &t, int64_t split_k, int64_t M, Plan *p) {
     auto allowed = [&](int i) { return forced < 0 || forced >= kShapes || i == forced; };
     auto blocks_of = [&](int i) {
         const TiledShape c = kTiledShapes[i];
-        return ((M + 16 * c.msw - 1) / (16 * c.msw)) * (int64_t)((t.Nt + 4 * c.nt - 1) / (4 * c.nt));
+        return ((M + 16 * c.msw - 1) / (16 * c.msw)) * tiled_col_blocks(t, c.nt);
     };
     // Whole K range: the shape that minimises (blocks per compute unit,
     // rounded up) x (block time relative to 128 x 256).
@@ -413,7 +421,7 @@ int make_tiled_plan(const Target &t, int64_t split_k, int64_t M, Plan *p) {
     if (best_i < 0) return fail(QLIN_ERR_UNSUPPORTED, "split_k=%d does not fit (workspace or counters)", (int)split_k);
     const TiledShape sh = kTiledShapes[best_i];
     const int Mt = (int)((M + 16 * sh.msw - 1) / (16 * sh.msw));
-    const int Gn = (t.Nt + 4 * sh.nt - 1) / (4 * sh.nt);
+    const int Gn = (int)tiled_col_blocks(t, sh.nt);
     p->path = kTiled;
     p->kern = kKernTiled;
     p->mrows = 16 * sh.msw;
@@ -546,39 +554,13 @@ int make_decode_plan(const Target &t, int path, int64_t split_k, int Mi, Plan *p
 int make_plan(const Target &t, int path, int64_t split_k, int64_t M, Plan *p) {
     if (path < kAuto || path > kRegs) return fail(QLIN_ERR_INVALID, "unknown path %d", path);
     if (split_k < 0 || split_k > t.Kb) return fail(QLIN_ERR_INVALID, "split_k must be in [0, K/128]");
-    if (path == kTiled || (path == kAuto && auto_tiled(M))) {
-        // the members' tiled launches run one after another and share the
-        // workspace: the plan reported is the widest member's
-        int wide = 0;
-        for (int i = 1; i < t.nmem; ++i) wide = t.mem[i]->Nt > t.mem[wide]->Nt ? i : wide;
-        Target one = t;
-        one.nmem = 1;
-        one.mem[0] = t.mem[wide];
-        one.N = t.mem[wide]->N;
-        one.Nt = t.mem[wide]->Nt;
-        return make_tiled_plan(one, split_k, M, p);
-    }
+    if (path == kTiled || (path == kAuto && auto_tiled(M))) return make_tiled_plan(t, split_k, M, p);
     return make_decode_plan(t, path, split_k, (int)std::min<int64_t>(M, kMaxSkinnyM), p);
 }
 
-// Workspace bytes the members' launches need for M rows under the target's
-// capacity (tiled: the largest member's; decode: the one launch's).
+// Workspace bytes the launch needs for M rows under the target's capacity.
 int workspace_need(const Target &t, int path, int64_t split_k, int64_t M, size_t *bytes) {
     *bytes = 0;
-    if (path == kTiled || (path == kAuto && auto_tiled(M))) {
-        for (int i = 0; i < t.nmem; ++i) {
-            Target one = t;
-            one.nmem = 1;
-            one.mem[0] = t.mem[i];
-            one.N = t.mem[i]->N;
-            one.Nt = t.mem[i]->Nt;
-            Plan p;
-            const int rc = make_tiled_plan(one, split_k, M, &p);
-            if (rc != QLIN_OK) return rc;
-            *bytes = std::max(*bytes, plan_ws_bytes(p));
-        }
-        return QLIN_OK;
-    }
     Plan p;
     const int rc = make_plan(t, path, split_k, M, &p);
     if (rc == QLIN_OK) *bytes = plan_ws_bytes(p);
@@ -668,38 +650,42 @@ int check_launch(const Target &t, int64_t M, const uint16_t *x, uint16_t *const 
 int launch_all(const Target &t, int path, int64_t split_k, int64_t M, const uint16_t *x, uint16_t *const *ys,
                void *ws, size_t ws_bytes, hipStream_t st) {
     if (path == kTiled || (path == kAuto && auto_tiled(M))) {
-        for (int i = 0; i < t.nmem; ++i) {
+        Plan p;
+        const int rc = make_tiled_plan(t, split_k, M, &p);
+        if (rc != QLIN_OK) return rc;
+        TiledArgs a;
+        a.x = x;
+        a.M = (int)M;
+        a.K = (int)t.K;
+        a.Kb = t.Kb;
+        a.Mt = (int)((M + p.mrows - 1) / p.mrows);
+        a.Gn = p.Gn;
+        a.S = p.S;
+        a.Kq = t.Kb / p.S;
+        a.Kr = t.Kb % p.S;
+        a.counters = (uint32_t *)ws;
+        a.ws = ws_partials(ws);
+        a.ws_bytes = ws_partial_bytes(ws, ws_bytes);
+        a.nmem = t.nmem;
+        int gb0 = 0;
+        for (int i = 0; i < kMaxMembers; ++i) {
+            TiledMember &f = a.mem[i];
+            if (i >= t.nmem) {         // absent: starts past the last column block, never selected
+                f = a.mem[0];
+                a.gb0[i] = p.Gn;
+                continue;
+            }
             const qlin_s *h = t.mem[i];
-            Target one = t;
-            one.nmem = 1;
-            one.mem[0] = h;
-            one.N = h->N;
-            one.Nt = h->Nt;
-            Plan p;
-            const int rc = make_tiled_plan(one, split_k, M, &p);
-            if (rc != QLIN_OK) return rc;
-            TiledArgs a;
-            a.codes = h->codes;
-            a.sz = h->sz;
-            a.x = x;
-            a.y = ys[i];
-            a.M = (int)M;
-            a.K = (int)h->K;
-            a.N = (int)h->N;
-            a.Kb = h->Kb;
-            a.Nt = h->Nt;
-            a.Mt = (int)((M + p.mrows - 1) / p.mrows);
-            a.Gn = p.Gn;
-            a.S = p.S;
-            a.Kq = h->Kb / p.S;
-            a.Kr = h->Kb % p.S;
-            a.counters = (uint32_t *)ws;
-            a.ws = ws_partials(ws);
-            a.ws_bytes = ws_partial_bytes(ws, ws_bytes);
-            const hipError_t e = launch_tiled(h->symmetric, TiledShape{p.mrows / 16, p.tn}, a, p.grid, st);
-            if (e != hipSuccess) return hip_fail(e, "tiled launch");
+            f.codes = h->codes;
+            f.sz = h->sz;
+            f.y = ys[i];
+            f.N = (int)h->N;
+            f.Nt = h->Nt;
+            a.gb0[i] = gb0;
+            gb0 += (h->Nt + 4 * p.tn - 1) / (4 * p.tn);
         }
-        return QLIN_OK;
+        const hipError_t e = launch_tiled(t.symmetric, TiledShape{p.mrows / 16, p.tn}, a, p.grid, st);
+        return e == hipSuccess ? QLIN_OK : hip_fail(e, "tiled launch");
     }
     for (int64_t m0 = 0; m0 < M;) {
         Plan p;
@@ -915,7 +901,7 @@ int plan_text(const Target &t, int path, int64_t split_k, int64_t M, char *buf, 
     const int rc = make_plan(t, path, split_k, M, &p);
     if (rc != QLIN_OK) return rc;
     const bool tiled = p.kern == kKernTiled;
-    const int64_t launches = tiled ? t.nmem : (M + p.rows - 1) / p.rows;
+    const int64_t launches = tiled ? 1 : (M + p.rows - 1) / p.rows;
     static const char *names[] = {"gemv", "regs", "skinny", "tiled"};
     snprintf(buf, (size_t)buflen, "path=%s kernel=%s grid=%d block=%d split=%d ranges=%d lds=%zu launches=%lld",
              names[p.kern], kernel_name(p.kern, p.mrows, p.tn, t.symmetric), p.grid,

@@ -79,19 +79,28 @@ constexpr TiledShape kTiledShapes[] = {{8, 4}, {4, 2}, {6, 4}};
 // owning half of every column group's tiles.
 constexpr int tiled_wsplit(TiledShape sh) { return sh.nt == 4 ? 2 : 1; }
 
-struct TiledArgs {
+// A tiled launch covers the column blocks of up to kMaxMembers linears that
+// share x: member i owns column blocks [gb0[i], gb0[i + 1]) and its column
+// tiles [0, Nt) are cut into blocks of 4 NT tiles from its first.
+struct TiledMember {
     const uint4 *codes;
     const void *sz;
-    const uint16_t *x;
-    uint16_t *y;
-    int M, K, N, Kb, Nt;
+    uint16_t *y;            // [M][N] bf16
+    int N, Nt;
+};
+struct TiledArgs {
+    const uint16_t *x;      // [M][K] bf16
+    int M, K, Kb;
     int Mt;                 // row blocks: ceil(M / (16 MSW))
-    int Gn;                 // column blocks: ceil(Nt / (4 NT))
+    int Gn;                 // column blocks over all members
     int S;                  // K chunks; chunk c holds Kq (+1 for c < Kr) groups
     int Kq, Kr;
     float *ws;              // S > 1: fp32 partial blocks, Gn Mt S of 16 MSW x 64 NT
     uint32_t *counters;     // S > 1: [Gn Mt] arrival counters, zero between launches
     uint32_t ws_bytes;      // size of ws
+    int nmem;
+    int gb0[kMaxMembers];   // first column block of each member (Gn for absent members)
+    TiledMember mem[kMaxMembers];
 };
 
 // Rows of x a SKINNY workgroup keeps in LDS for M rows (M <= 64): the next

@@ -15,7 +15,9 @@ namespace qlin {
 // ---- TILED: prefill-sized M (GEMM), matrix-core dequantization ----------
 //
 // A workgroup of 4 WS waves computes a BM x BN = 16 MSW x 64 NT block of y:
-// rows [BM im, BM im + BM), column tiles [4 NT jn, 4 NT jn + 4 NT).  Wave w
+// rows [BM im, BM im + BM), column tiles [4 NT j, 4 NT j + 4 NT) of one
+// member of the launch (column block jn of all members is block j of the
+// member that owns it).  Wave w
 // owns all BM rows (MSW m-subtiles of 16) of the NW = NT / WS tiles NW w + t:
 // each tile is dequantized once per workgroup and every dequantized operand
 // feeds MSW matrix products.  With WS = 2 two waves share each SIMD, so the
@@ -77,8 +79,19 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     const int item = xcd * per + min(xcd, rem) + q;
     const int blk = SPLIT ? item / a.S : item;        // once per workgroup
     const int c = SPLIT ? item - blk * a.S : 0;
-    const int jn = blk / a.Mt;
+    const int jn = blk / a.Mt;                        // column block over all members
     const int im = blk - jn * a.Mt;
+    // the member owning column block jn (every index of the argument arrays
+    // static but one, see wg_work in kernels.hip) and its tiles [t0, t0 + 4 NT)
+    int m = 0, gb = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxMembers; ++i)
+        if (jn >= a.gb0[i]) {
+            m = i;
+            gb = a.gb0[i];
+        }
+    const TiledMember &f = a.mem[m];
+    const int Nt = f.Nt;
     const int g0 = SPLIT ? c * a.Kq + min(c, a.Kr) : 0;   // the chunk's groups [g0, g1]
     const int g1 = SPLIT ? g0 + a.Kq + (c < a.Kr ? 1 : 0) - 1 : a.Kb - 1;
     const int lm = lane & 15, lg = lane >> 4;
@@ -116,16 +129,16 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     // tile), through resources based at the workgroup's first tile (its
     // blocks span at most 16 Kb KiB); wv / sv = byte offsets of this lane's
     // part of block (tile, 0)
-    const int t0 = jn * kTiles, ntw = min(kTiles, a.Nt - t0);
+    const int t0 = (jn - gb) * kTiles, ntw = min(kTiles, Nt - t0);
     constexpr uint32_t kSzBlk = SYM ? kTileN * 2 : kTileN * 4;          // s|z bytes per block
     const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)(a.codes + (size_t)t0 * a.Kb * 64), 0, ntw * a.Kb * 1024, kRsrcFlags);
+        (void *)(f.codes + (size_t)t0 * a.Kb * 64), 0, ntw * a.Kb * 1024, kRsrcFlags);
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-        (void *)((const char *)a.sz + (size_t)t0 * a.Kb * kSzBlk), 0, ntw * a.Kb * (int)kSzBlk, kRsrcFlags);
+        (void *)((const char *)f.sz + (size_t)t0 * a.Kb * kSzBlk), 0, ntw * a.Kb * (int)kSzBlk, kRsrcFlags);
     uint32_t wv[NW], sv[NW];
 #pragma unroll
     for (int u = 0; u < NW; ++u) {
-        const uint32_t tr = (uint32_t)(min(t0 + wave * NW + u, a.Nt - 1) - t0) * (uint32_t)a.Kb;   // block (tile, 0)
+        const uint32_t tr = (uint32_t)(min(t0 + wave * NW + u, Nt - 1) - t0) * (uint32_t)a.Kb;   // block (tile, 0)
         wv[u] = tr * 1024u + lane * 16u;
         // 2-byte scales: one dword per lane covers columns 2i, 2i + 1 (read_w picks the half)
         sv[u] = tr * kSzBlk + (SYM ? (lane & 7) : lm) * 4u;
@@ -282,11 +295,11 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
         if (row >= a.M) continue;
 #pragma unroll
         for (int t = 0; t < NW; ++t) {
-            const int tt = jn * kTiles + wave * NW + t;
-            if (tt >= a.Nt) continue;
+            const int tt = t0 + wave * NW + t;
+            if (tt >= Nt) continue;
             const v4f v = acc[ms][t];
             const uint2 o = make_uint2(cvt_pk_bf16(v[0], v[1]), cvt_pk_bf16(v[2], v[3]));
-            *(uint2 *)(a.y + (size_t)row * a.N + (size_t)tt * kTileN + 4 * lg) = o;
+            *(uint2 *)(f.y + (size_t)row * f.N + (size_t)tt * kTileN + 4 * lg) = o;
         }
     }
 }

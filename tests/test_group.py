@@ -75,6 +75,24 @@ def test_qkv_group_matches_oracle(qkv, M):
     check_members(group_run(lins, x, ws_bytes=0), ws, x, what=f"M={M} no workspace")
 
 
+@pytest.mark.parametrize("M", [65, 128, 300, 2048])
+def test_qkv_group_at_prefill_rows(qkv, M):
+    """Prefill rows: one tiled launch over the three members (q's 16-tile
+    column blocks, then k's, then v's), with and without a workspace for the
+    K split; all outputs compared (sampled columns at M = 2048)."""
+    ws, lins = qkv
+    x = gen.model_activations(4, M, ws[0]["K"])
+    need, plan = qlin.group_plan(lins, M)
+    assert "path=tiled" in plan and "launches=1" in plan, plan
+    for nb in (-1, 0):
+        ys = group_run(lins, x, ws_bytes=nb)
+        for i, (y, w) in enumerate(zip(ys, ws)):
+            cols = np.arange(w["N"]) if M < 2048 else np.unique(np.r_[0:64, w["N"] - 64:w["N"], 200:w["N"]:97])
+            y_ref = ref.forward(x, w["packed"][cols], w["scales"][cols], w["zeros"][cols])
+            r = ref.compare(np.ascontiguousarray(y[:, cols]), y_ref)
+            assert r["ok"], f"M={M} member {i} workspace={nb}: {r}"
+
+
 def test_qkv_group_is_one_launch(qkv):
     _, lins = qkv
     if torch.cuda.get_device_properties(0).multi_processor_count != 256:
