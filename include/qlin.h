@@ -135,8 +135,9 @@ int qlin_forward(qlin_t h, int64_t M, const uint16_t *x, uint16_t *y, void *stre
  * K-chunks (split_k; 0 = the planner's choice) forced, for tests and tuning.
  * Errors as qlin_forward, plus INVALID for an unknown path, split_k < 0 or
  * split_k > K/128, and UNSUPPORTED when the path cannot run this M
- * (GEMV: M <= 4; REGS: M <= 16; SKINNY: M <= 64; TILED: M * K < 2^31) or
- * the forced split does not fit LDS or the handle's workspace.
+ * (GEMV: M <= 4; REGS: M <= 16; SKINNY: M <= 64) or the forced split does
+ * not fit LDS or the handle's workspace.  The TILED path takes any M: rows
+ * beyond M * K < 2^31 run as further launches.
  */
 int qlin_forward_path(qlin_t h, int path, int64_t split_k, int64_t M,
                       const uint16_t *x, uint16_t *y, void *stream);

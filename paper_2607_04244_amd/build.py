@@ -1,7 +1,11 @@
 """Build the HIP library ``libqlin.so`` in-tree for gfx950 with hipcc.
 
 ``python -m paper_2607_04244_amd.build`` (or ``__graft_entry__.build()``)
-compiles every source under ``csrc/`` on each call.
+compiles every source under ``csrc/`` on each call.  It also links
+``libqlin_asan.so``: the same device code, with the host-only C-ABI sources
+(argument checks, planner, handle management) compiled by g++ with
+AddressSanitizer and UndefinedBehaviorSanitizer, for the CPU tests of the
+ABI (the sanitizer runtimes are preloaded into the Python that loads it).
 """
 
 import os
@@ -16,6 +20,9 @@ LIB = os.path.join(HERE, "libqlin.so")
 # softmax rescaling), which would otherwise go through AGPR copies.
 SOURCES = [("kernels.hip", []), ("tiled.hip", ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]), ("attn.hip", ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]),
            ("qlin.cpp", []), ("attn_abi.cpp", [])]
+HOST_SOURCES = ("qlin.cpp", "attn_abi.cpp")       # no device code: plain C++ against the HIP headers
+LIB_ASAN = os.path.join(HERE, "libqlin_asan.so")
+SANITIZE = ["-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer"]
 ARCH = "gfx950"
 
 # Packed-fp32 vector instructions are switched off in the device pass; the
@@ -54,14 +61,27 @@ def build(verbose=False, extra_flags=()):
             print(_errs(r), file=sys.stderr)
     if failed:
         raise RuntimeError("hipcc failed:\n" + "\n".join(failed))
-    tmp = LIB + ".tmp"
-    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
-    r = subprocess.run(cmd, capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"link failed ({r.returncode}):\n{_errs(r)}")
-    for o in objs:
+    # the host sources again, instrumented, for the sanitizer library
+    cxx = os.environ.get("CXX_HOST", "g++")
+    asan_objs = []
+    for src in HOST_SOURCES:
+        obj = os.path.join(CSRC, os.path.splitext(src)[0] + ".asan.o")
+        cmd = [cxx, "-O1", "-g", "-std=c++17", "-fPIC", *SANITIZE, "-D__HIP_PLATFORM_AMD__",
+               "-I", "/opt/rocm/include", *inc, "-c", os.path.join(CSRC, src), "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"{cxx} failed on {src}:\n{r.stderr}")
+        asan_objs.append(obj)
+    device_objs = [o for (src, _), o in zip(SOURCES, objs) if src not in HOST_SOURCES]
+    for out, parts in ((LIB, objs), (LIB_ASAN, device_objs + asan_objs)):
+        tmp = out + ".tmp"
+        cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *parts, "-o", tmp]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"link failed ({r.returncode}):\n{_errs(r)}")
+        os.replace(tmp, out)
+    for o in objs + asan_objs:
         os.remove(o)
-    os.replace(tmp, LIB)
     return LIB
 
 

@@ -365,7 +365,14 @@ int64_t tiled_col_blocks(const Target &t, int nt) {
 // rows would leave part of the chip idle, 128 x 256 otherwise.
 int make_tiled_plan(const Target &t, int64_t split_k, int64_t M, Plan *p) {
     if (split_k < 0 || split_k > t.Kb) return fail(QLIN_ERR_INVALID, "split_k must be in [0, K/128]");
-    if (M * t.K >= ((int64_t)1 << 31)) return fail(QLIN_ERR_UNSUPPORTED, "TILED path needs M * K < 2^31");
+    // one launch addresses x with 32-bit byte offsets: more rows than M * K
+    // < 2^31 allows run as launches of that many rows each
+    const int64_t rows = std::min<int64_t>(M, (((int64_t)1 << 31) - 1) / t.K);
+    if (rows < M) {
+        const int rc = make_tiled_plan(t, split_k, rows, p);
+        p->rows = (int)rows;
+        return rc;
+    }
     constexpr int kShapes = (int)(sizeof kTiledShapes / sizeof kTiledShapes[0]);
     static const int forced = [] {                   // tuning knob: QLIN_TILED_SHAPE = index into kTiledShapes
         const char *e = getenv("QLIN_TILED_SHAPE");
@@ -645,60 +652,70 @@ int check_launch(const Target &t, int64_t M, const uint16_t *x, uint16_t *const 
     return QLIN_OK;
 }
 
+// One tiled launch of plan p over M rows (M * K < 2^31) at x, member i
+// writing ys[i].
+int launch_tiled_rows(const Target &t, const Plan &p, int64_t M, const uint16_t *x, uint16_t *const *ys,
+                      void *ws, size_t ws_bytes, hipStream_t st) {
+    TiledArgs a;
+    a.x = x;
+    a.M = (int)M;
+    a.K = (int)t.K;
+    a.Kb = t.Kb;
+    a.Mt = (int)((M + p.mrows - 1) / p.mrows);
+    a.Gn = p.Gn;
+    a.S = p.S;
+    a.Kq = t.Kb / p.S;
+    a.Kr = t.Kb % p.S;
+    a.counters = (uint32_t *)ws;
+    a.ws = ws_partials(ws);
+    a.ws_bytes = ws_partial_bytes(ws, ws_bytes);
+    a.nmem = t.nmem;
+    int gb0 = 0;
+    for (int i = 0; i < kMaxMembers; ++i) {
+        TiledMember &f = a.mem[i];
+        if (i >= t.nmem) {             // absent: starts past the last column block, never selected
+            f = a.mem[0];
+            a.gb0[i] = p.Gn;
+            continue;
+        }
+        const qlin_s *h = t.mem[i];
+        f.codes = h->codes;
+        f.sz = h->sz;
+        f.y = ys[i];
+        f.N = (int)h->N;
+        f.Nt = h->Nt;
+        a.gb0[i] = gb0;
+        gb0 += (h->Nt + 4 * p.tn - 1) / (4 * p.tn);
+    }
+    const hipError_t e = launch_tiled(t.symmetric, TiledShape{p.mrows / 16, p.tn}, a, p.grid, st);
+    return e == hipSuccess ? QLIN_OK : hip_fail(e, "tiled launch");
+}
+
 // Runs M rows through the members of t with the workspace (ws, ws_bytes)
-// (capacity already set in t).  Arguments are checked by the caller.
+// (capacity already set in t), in launches of the plan's rows each (a
+// shorter last one has a plan of its own).  Arguments are checked by the
+// caller.
 int launch_all(const Target &t, int path, int64_t split_k, int64_t M, const uint16_t *x, uint16_t *const *ys,
                void *ws, size_t ws_bytes, hipStream_t st) {
-    if (path == kTiled || (path == kAuto && auto_tiled(M))) {
-        Plan p;
-        const int rc = make_tiled_plan(t, split_k, M, &p);
-        if (rc != QLIN_OK) return rc;
-        TiledArgs a;
-        a.x = x;
-        a.M = (int)M;
-        a.K = (int)t.K;
-        a.Kb = t.Kb;
-        a.Mt = (int)((M + p.mrows - 1) / p.mrows);
-        a.Gn = p.Gn;
-        a.S = p.S;
-        a.Kq = t.Kb / p.S;
-        a.Kr = t.Kb % p.S;
-        a.counters = (uint32_t *)ws;
-        a.ws = ws_partials(ws);
-        a.ws_bytes = ws_partial_bytes(ws, ws_bytes);
-        a.nmem = t.nmem;
-        int gb0 = 0;
-        for (int i = 0; i < kMaxMembers; ++i) {
-            TiledMember &f = a.mem[i];
-            if (i >= t.nmem) {         // absent: starts past the last column block, never selected
-                f = a.mem[0];
-                a.gb0[i] = p.Gn;
-                continue;
-            }
-            const qlin_s *h = t.mem[i];
-            f.codes = h->codes;
-            f.sz = h->sz;
-            f.y = ys[i];
-            f.N = (int)h->N;
-            f.Nt = h->Nt;
-            a.gb0[i] = gb0;
-            gb0 += (h->Nt + 4 * p.tn - 1) / (4 * p.tn);
-        }
-        const hipError_t e = launch_tiled(t.symmetric, TiledShape{p.mrows / 16, p.tn}, a, p.grid, st);
-        return e == hipSuccess ? QLIN_OK : hip_fail(e, "tiled launch");
-    }
+    const bool tiled = path == kTiled || (path == kAuto && auto_tiled(M));
     for (int64_t m0 = 0; m0 < M;) {
         Plan p;
-        const int rc = make_plan(t, path, split_k, M - m0, &p);
+        int rc = tiled ? make_tiled_plan(t, split_k, M - m0, &p) : make_plan(t, path, split_k, M - m0, &p);
         if (rc != QLIN_OK) return rc;
         const int64_t Ms = std::min<int64_t>(p.rows, M - m0);
-        if (Ms != p.rows) {            // a shorter last slice has a plan of its own
-            const int rc2 = make_plan(t, path, split_k, Ms, &p);
-            if (rc2 != QLIN_OK) return rc2;
+        if (Ms != p.rows) {
+            rc = tiled ? make_tiled_plan(t, split_k, Ms, &p) : make_plan(t, path, split_k, Ms, &p);
+            if (rc != QLIN_OK) return rc;
         }
-        const FwdArgs a = fwd_args(t, p, Ms, x, ys, ws, ws_bytes, m0);
-        const hipError_t e = launch_forward(p.kern, p.mrows, p.tn, t.symmetric, p.grid, p.lds, a, st);
-        if (e != hipSuccess) return hip_fail(e, "forward launch");
+        if (tiled) {
+            uint16_t *yk[kMaxMembers];
+            for (int i = 0; i < t.nmem; ++i) yk[i] = ys[i] + m0 * t.mem[i]->N;
+            if ((rc = launch_tiled_rows(t, p, Ms, x + m0 * t.K, yk, ws, ws_bytes, st)) != QLIN_OK) return rc;
+        } else {
+            const FwdArgs a = fwd_args(t, p, Ms, x, ys, ws, ws_bytes, m0);
+            const hipError_t e = launch_forward(p.kern, p.mrows, p.tn, t.symmetric, p.grid, p.lds, a, st);
+            if (e != hipSuccess) return hip_fail(e, "forward launch");
+        }
         m0 += Ms;
     }
     return QLIN_OK;
@@ -901,7 +918,7 @@ int plan_text(const Target &t, int path, int64_t split_k, int64_t M, char *buf, 
     const int rc = make_plan(t, path, split_k, M, &p);
     if (rc != QLIN_OK) return rc;
     const bool tiled = p.kern == kKernTiled;
-    const int64_t launches = tiled ? 1 : (M + p.rows - 1) / p.rows;
+    const int64_t launches = (M + p.rows - 1) / p.rows;
     static const char *names[] = {"gemv", "regs", "skinny", "tiled"};
     snprintf(buf, (size_t)buflen, "path=%s kernel=%s grid=%d block=%d split=%d ranges=%d lds=%zu launches=%lld",
              names[p.kern], kernel_name(p.kern, p.mrows, p.tn, t.symmetric), p.grid,

@@ -12,7 +12,9 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libqlin.so")
+# QLIN_LIB selects another build of the same library (the sanitizer build of
+# the CPU tests); by default the in-tree libqlin.so
+LIB_PATH = os.environ.get("QLIN_LIB") or os.path.join(_HERE, "libqlin.so")
 
 QLIN_OK = 0
 QLIN_ERR_INVALID = -1

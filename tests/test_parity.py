@@ -472,3 +472,26 @@ def test_automatic_plan_for_decoder_shapes(M, K, N, kernel, split):
     plan = lin.plan(M)
     lin.close()
     assert f"kernel={kernel} " in plan and f"split={split} " in plan, plan
+
+
+def test_rows_beyond_32_bit_offsets_of_x():
+    """M * K = 2^31 (K = 65536, M = 32768: a 4 GiB x) through the automatic
+    plan: the tiled kernel addresses x with 32-bit byte offsets, so the rows
+    run as two launches (32767 rows, then one).  x is drawn on the device
+    (seeded); the rows checked, on both sides of the boundary, are read back
+    and compared with the oracle on every column."""
+    K, N, M = 65536, 64, 32768
+    c = gen.random_case(12, 1, K, N)
+    lin = make(c)
+    g = torch.Generator(device="cuda").manual_seed(12)
+    x = torch.randn((M, K), device="cuda", generator=g).to(torch.bfloat16)
+    y = lin.forward(x)
+    torch.cuda.synchronize()
+    assert "launches=2" in lin.plan(M), lin.plan(M)
+    rows = np.array([0, 1, 4095, 32766, 32767])
+    xr = host_bits(x[torch.from_numpy(rows).cuda()])
+    y_ref = ref.forward(xr, c["packed"], c["scales"], c["zeros"])
+    assert_close(np.ascontiguousarray(host_bits(y)[rows]), y_ref, f"K={K} M={M} rows {rows}")
+    del x, y
+    torch.cuda.empty_cache()
+    lin.close()
