@@ -76,11 +76,39 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     const int xcd = blockIdx.x & 7, q = blockIdx.x >> 3;
     const int nitem = a.Gn * a.Mt * (SPLIT ? a.S : 1), per = nitem >> 3, rem = nitem & 7;
     if (q >= per + (xcd < rem ? 1 : 0)) return;      // uniform: padding of the grid
-    const int item = xcd * per + min(xcd, rem) + q;
-    const int blk = SPLIT ? item / a.S : item;        // once per workgroup
-    const int c = SPLIT ? item - blk * a.S : 0;
-    const int jn = blk / a.Mt;                        // column block over all members
-    const int im = blk - jn * a.Mt;
+    const int s0 = xcd * per + min(xcd, rem);        // the XCD's run of items
+    int blk, c = 0, jn, im;
+    if constexpr (SPLIT) {
+        const int item = s0 + q;
+        blk = item / a.S;                             // once per workgroup
+        c = item - blk * a.S;
+        jn = blk / a.Mt;                              // column block over all members
+        im = blk - jn * a.Mt;
+    } else {
+        // the run's blocks (column blocks ja .. jb: rows r0 .. of ja, all of
+        // the ones between, rows .. r1 of jb) are taken row block by row
+        // block, so the workgroups running together on the XCD share their x
+        // rows in its L2 as well as their weights
+        const int last = s0 + per + (xcd < rem ? 1 : 0) - 1;
+        const int ja = s0 / a.Mt, jb = last / a.Mt;
+        const int r0 = s0 - ja * a.Mt, r1 = last - jb * a.Mt;
+        if (ja == jb) {
+            jn = ja;
+            im = r0 + q;
+        } else {
+            const int mid = jb - ja - 1;
+            auto before = [&](int i) { return i * mid + max(0, i - r0) + min(i, r1 + 1); };   // items in rows < i
+            int lo = 0, hi = a.Mt - 1;                // the row holding the q-th item
+            while (lo < hi) {
+                const int md = (lo + hi + 1) >> 1;
+                if (before(md) <= q) lo = md;
+                else hi = md - 1;
+            }
+            im = lo;
+            jn = (im >= r0 ? ja : ja + 1) + (q - before(im));
+        }
+        blk = jn * a.Mt + im;
+    }
     // the member owning column block jn (every index of the argument arrays
     // static but one, see wg_work in kernels.hip) and its tiles [t0, t0 + 4 NT)
     int m = 0, gb = 0;
