@@ -21,7 +21,9 @@ rest of the metric, measured in the same run: the M=1 linear (K=N=2560,
 GB/s) and the 36-layer 4B-shaped weight pass at M=16 (microseconds per
 verification step and per layer: q|k|v as one grouped launch, then o,
 gate|up and down, 144 launches in one graph on one stream, so each runs after
-the previous one as in a decoder), and the drafter's 5-layer pass.
+the previous one as in a decoder), and the drafter's 5-layer pass, each next
+to the same launch structure reduced to plain streaming reads of each
+launch's bytes (the ceiling of a pass made of that many dependent launches).
 
 Other modes (not the benchmark line): ``--workload`` c0 | c2m1 | c2m4 |
 c2m8 | c2m16 | model (the 36-layer pass at M=16) | drafter (the drafter's
@@ -209,13 +211,37 @@ def calibrate_copy():
                       "bytes_written_per_launch": 1 << 28, "launches": 20}), flush=True)
 
 
-def model_pass(M=16, x_seed=3, separate_qkv=False, drafter=False, reps=15):
+def structure_ceiling_us(torch, qlin, sizes, stream, reps):
+    """The same launch structure with nothing but the weight stream: one plain
+    streaming read per launch of that launch's bytes, from distinct regions of
+    one buffer, in one graph.  Returns the step time (us)."""
+    offs, total = [], 0
+    for n in sizes:
+        offs.append(total)
+        total += (n + 4095) // 4096 * 4096
+    buf = torch.empty(total, dtype=torch.uint8, device="cuda").fill_(1)
+    sink = torch.zeros(4096, dtype=torch.int32, device="cuda")
+    best = None
+    for grid in (256, 512, 1024):
+        calls = [(lambda o=o, n=n: qlin.qlin_stream_read(buf.data_ptr() + o, (n + 15) // 16 * 16, grid,
+                                                          sink.data_ptr(), stream.cuda_stream))
+                 for o, n in zip(offs, sizes)]
+        us, g = graph_time_us(torch, stream, calls, reps=reps)
+        del g
+        best = us * len(sizes) if best is None else min(best, us * len(sizes))
+    del buf
+    torch.cuda.empty_cache()
+    return best
+
+
+def model_pass(M=16, x_seed=3, separate_qkv=False, drafter=False, reps=15, ceiling=False):
     """The linears of a whole decoder step at M rows, one graph on one stream:
     per layer q|k|v (one grouped launch, or three), o, gate|up, down.  The
     target: 36 layers of config-3 weights (asymmetric).  The drafter: its 5
     layers and its context projection (symmetric, Sec. 3.3).  Prefill-sized
     M share one caller workspace sized for the largest plan.  Returns a dict
-    of the step time and rates."""
+    of the step time and rates; with ``ceiling``, also the step time of the
+    same launches reduced to plain streaming reads of their bytes."""
     import torch
 
     from paper_2607_04244_amd import qlin
@@ -238,13 +264,14 @@ def model_pass(M=16, x_seed=3, separate_qkv=False, drafter=False, reps=15):
         w = gen.drafter_linear(0, len(gen.LAYER_SHAPES))
         layers.insert(0, [qlin.QLinear(w["packed"], w["scales"], None)])
     setup_s = time.perf_counter() - t0
-    steps = []
+    steps, launch_bytes = [], []
     for grp in layers:
         K = grp[0].K
         if K not in xs:
             xs[K] = torch.from_numpy(gen.model_activations(x_seed, M, K).view(np.int16)).view(torch.bfloat16).cuda()
         ys = [torch.empty((M, l.N), dtype=torch.bfloat16, device="cuda") for l in grp]
         steps.append((grp, ys))
+        launch_bytes.append(sum(algorithmic_bytes(M, K, l.N, symmetric=drafter) for l in grp))
         for l in grp:
             total += algorithmic_bytes(M, K, l.N, symmetric=drafter)
             flops += 2 * M * K * l.N
@@ -264,12 +291,17 @@ def model_pass(M=16, x_seed=3, separate_qkv=False, drafter=False, reps=15):
     torch.cuda.empty_cache()
     who = (f"drafter: {n_layers} layers + context projection, symmetric" if drafter
            else f"36-layer 4B decoder weight pass")
-    return {"workload": f"{who}, M={M} ({len(calls)} launches, "
-                        f"{'separate' if separate_qkv else 'grouped'} q|k|v, one graph)",
-            "us_per_step": round(us_step, 2), "us_per_layer": round(us_step / n_layers, 3),
-            "bytes_per_step": total, "GBps": round(gbs, 1), "pct_of_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2),
-            "TFLOPs": round(tfs, 1), "mfma_util_pct": round(100 * tfs / PEAK_BF16_TFLOPS, 2),
-            "workspace_bytes": need, "setup_s": round(setup_s, 1), "plans": plans}
+    out = {"workload": f"{who}, M={M} ({len(calls)} launches, "
+                       f"{'separate' if separate_qkv else 'grouped'} q|k|v, one graph)",
+           "us_per_step": round(us_step, 2), "us_per_layer": round(us_step / n_layers, 3),
+           "bytes_per_step": total, "GBps": round(gbs, 1), "pct_of_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2),
+           "TFLOPs": round(tfs, 1), "mfma_util_pct": round(100 * tfs / PEAK_BF16_TFLOPS, 2),
+           "workspace_bytes": need, "setup_s": round(setup_s, 1), "plans": plans}
+    if ceiling:
+        c_us = structure_ceiling_us(torch, qlin, launch_bytes, stream, reps)
+        out["stream_read_structure_us"] = round(c_us, 2)
+        out["pct_of_stream_read_structure"] = round(100 * c_us / us_step, 1)
+    return out
 
 
 def bench_model(args, M=16, x_seed=3, drafter=False):
@@ -503,17 +535,19 @@ def main():
         # the whole 4B-shaped step (and the drafter's) at M=16
         print("measuring the M=1 linear and the model passes", file=sys.stderr, flush=True)
         c0 = linear_rate(make_case("c0"), 2000, 100)
-        model = model_pass(16)
-        draft = model_pass(16, drafter=True)
+        model = model_pass(16, ceiling=True)
+        draft = model_pass(16, drafter=True, ceiling=True)
         parts = {"M1_K2560_N2560": {"us": round(c0["ms_step"] * 1e3, 3), "GBps": round(c0["GBps"], 1),
                                     "pct_of_peak_hbm": round(100 * c0["GBps"] / PEAK_HBM_GBS, 2),
                                     "plan": c0["plan"]},
                  "M16_K2560_N19456": {"us": round(ms_step * 1e3, 3), "GBps": round(gbs, 1),
                                       "pct_of_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2)},
                  "model_M16": {k: model[k] for k in ("workload", "us_per_step", "us_per_layer", "GBps",
-                                                     "pct_of_peak_hbm", "bytes_per_step")},
+                                                     "pct_of_peak_hbm", "bytes_per_step", "stream_read_structure_us",
+                                                     "pct_of_stream_read_structure")},
                  "drafter_M16": {k: draft[k] for k in ("workload", "us_per_step", "us_per_layer", "GBps",
-                                                       "pct_of_peak_hbm", "bytes_per_step")}}
+                                                       "pct_of_peak_hbm", "bytes_per_step", "stream_read_structure_us",
+                                                       "pct_of_stream_read_structure")}}
         parts["model_M16"]["us_at_70pct_of_peak"] = round(model["bytes_per_step"] / (0.7 * PEAK_HBM_GBS * 1e3), 1)
 
     kernel = plan.split("kernel=")[1].split()[0] if "kernel=" in plan else "?"
