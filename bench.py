@@ -102,6 +102,68 @@ def traffic_from_profiles(kernel, key=None):
     return e.get("hbm_bytes_per_launch")
 
 
+class ClockSampler:
+    """Samples the GPU's current shader (sclk) and memory (mclk) clocks from
+    the driver's sysfs tables (the row marked with '*') in a thread, for the
+    timed region; summary: min / median / max MHz over the samples, and the
+    table's rows.  Absent tables give an empty summary."""
+
+    def __init__(self, period_s=0.0005):
+        import glob
+        import threading
+        self.period = period_s
+        self.paths = {}
+        for kind in ("sclk", "mclk"):
+            found = sorted(glob.glob(f"/sys/class/drm/card*/device/pp_dpm_{kind}"))
+            if found:
+                self.paths[kind] = found[0]
+        self.samples = {k: [] for k in self.paths}
+        self.levels = {k: self._read(k)[1] for k in self.paths}
+        self._stop = threading.Event()
+        self._thread = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self, kind):
+        try:
+            lines = open(self.paths[kind]).read().split("\n")
+        except OSError:
+            return None, []
+        cur, levels = None, []
+        for line in lines:
+            parts = line.replace("Mhz", "").replace("MHz", "").split()
+            if len(parts) >= 2 and parts[1].isdigit():
+                levels.append(int(parts[1]))
+                if line.strip().endswith("*"):
+                    cur = int(parts[1])
+        return cur, levels
+
+    def _run(self):
+        while not self._stop.is_set():
+            for k in self.paths:
+                cur = self._read(k)[0]
+                if cur is not None:
+                    self.samples[k].append(cur)
+            time.sleep(self.period)
+
+    def __enter__(self):
+        if self.paths:
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self._thread.is_alive():
+            self._thread.join()
+
+    def summary(self):
+        out = {}
+        for k, v in self.samples.items():
+            if v:
+                v = sorted(v)
+                out[f"{k}_mhz"] = {"min": v[0], "median": v[len(v) // 2], "max": v[-1], "samples": len(v)}
+                out[f"{k}_levels_mhz"] = self.levels.get(k, [])
+        return out
+
+
 def host_cores():
     """Cores this process may run on (its affinity mask)."""
     try:
@@ -454,14 +516,15 @@ def linear_rate(case, steps, warmup, path=0, split=0):
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    with torch.cuda.stream(stream):
-        ev0.record(stream)
-        for _ in range(steps // R):
-            g_full.replay()
-        if g_tail is not None:
-            g_tail.replay()
-        ev1.record(stream)
-    stream.synchronize()
+    with ClockSampler() as clocks:
+        with torch.cuda.stream(stream):
+            ev0.record(stream)
+            for _ in range(steps // R):
+                g_full.replay()
+            if g_tail is not None:
+                g_tail.replay()
+            ev1.record(stream)
+        stream.synchronize()
     torch.cuda.synchronize()
     ms_step = ev0.elapsed_time(ev1) / steps
     gbs = bytes_step / (ms_step * 1e-3) / 1e9
@@ -483,7 +546,7 @@ def linear_rate(case, steps, warmup, path=0, split=0):
     del lins
     torch.cuda.empty_cache()
     return {"ms_step": ms_step, "GBps": gbs, "plan": plan, "R": R, "bytes": bytes_step, "eager_us": eager_us,
-            "stream": stream}
+            "stream": stream, "clocks": clocks.summary()}
 
 
 def main():
@@ -573,7 +636,8 @@ def main():
                    "us_per_step": round(ms_step * 1e3, 3), "pct_of_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2),
                    "stream_read_ceiling_GBps": round(ceil_gbs, 1), "stream_read_ceiling_us": round(ceil_us, 3),
                    "pct_of_stream_read_ceiling": round(100 * gbs / ceil_gbs, 1),
-                   "eager_launch_us_per_step": round(eager_us, 3)},
+                   "eager_launch_us_per_step": round(eager_us, 3),
+                   "clocks_during_timed_region": r["clocks"]},
         "metric_parts": parts,
         "roofline": {"bound": "hbm", "kernel": kernel, "achieved": round(gbs, 2), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
