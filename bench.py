@@ -248,6 +248,18 @@ def stream_read_ceiling(torch, qlin, nbytes, stream):
     return nb / (best * 1e-6) / 1e9, best
 
 
+def launch_floor_us(torch, qlin, stream, n=200):
+    """The per-launch cost of the launch structure itself: n back-to-back
+    launches of the streaming-read kernel over 16 bytes (256 workgroups of 512
+    threads, the decode kernels' launch shape), replayed from one graph."""
+    buf = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(4096, dtype=torch.int32, device="cuda")
+    calls = [(lambda: qlin.qlin_stream_read(buf.data_ptr(), 16, 256, sink.data_ptr(), stream.cuda_stream))] * n
+    us, g = graph_time_us(torch, stream, calls, reps=10)
+    del g
+    return us
+
+
 def make_case(workload):
     from synth import gen
     if workload == "verify":
@@ -591,6 +603,7 @@ def main():
     ms_step, gbs, plan, R, bytes_step, eager_us = r["ms_step"], r["GBps"], r["plan"], r["R"], r["bytes"], r["eager_us"]
     K_steps = args.steps
     ceil_gbs, ceil_us = stream_read_ceiling(torch, qlin, bytes_step, r["stream"])
+    floor_us = launch_floor_us(torch, qlin, r["stream"])
 
     parts = None
     if args.workload == "verify" and not args.no_parts:
@@ -636,6 +649,9 @@ def main():
                    "us_per_step": round(ms_step * 1e3, 3), "pct_of_peak_hbm": round(100 * gbs / PEAK_HBM_GBS, 2),
                    "stream_read_ceiling_GBps": round(ceil_gbs, 1), "stream_read_ceiling_us": round(ceil_us, 3),
                    "pct_of_stream_read_ceiling": round(100 * gbs / ceil_gbs, 1),
+                   "launch_floor_us": round(floor_us, 3),
+                   "launch_floor_bound_pct_of_peak_hbm": round(
+                       100 * bytes_step / ((floor_us + bytes_step / (PEAK_HBM_GBS * 1e3)) * 1e-6) / 1e9 / PEAK_HBM_GBS, 1),
                    "eager_launch_us_per_step": round(eager_us, 3),
                    "clocks_during_timed_region": r["clocks"]},
         "metric_parts": parts,
