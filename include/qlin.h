@@ -101,7 +101,8 @@ qlin_t qlin_create_symmetric(int64_t K, int64_t N, int64_t group,
  *   zeros   DEVICE bf16 [N][K/group] integers in [0, 15], or NULL for the
  *           symmetric format (z = 8)
  *   packed  DEVICE uint32 [N][K/8] output in qlin_create's layout, 4-byte
- *           aligned, must not overlap w
+ *           aligned (16-byte aligned is written with 16-byte stores, faster),
+ *           must not overlap w
  *   stream  hipStream_t; NULL = the default stream
  *
  * Shape rules as qlin_create.  Asynchronous.  Errors: INVALID (shape, NULL,

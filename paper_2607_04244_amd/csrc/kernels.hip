@@ -802,40 +802,95 @@ __global__ void __launch_bounds__(kThreads) k_gemv4(FwdArgs a) {
 // RTN quantizer):  code = clamp(rint(w / s) + z, 0, 15), quotient in binary32
 // with a correctly rounded division, nearest integer with ties to even, a
 // NaN quotient gives z; code k = 8j + i goes to bits [4i, 4i + 4) of word j.
-// One thread per output word: a 16-byte load of 8 weights, one 4-byte store.
-template <bool SYM>
-__global__ void k_quantize_pack(const uint4 *__restrict__ w, const uint16_t *__restrict__ scales,
-                                const uint16_t *__restrict__ zeros, uint32_t *__restrict__ packed, int K, int N) {
-    const int K8 = K / 8, Kg = K / kGroup;
-    const size_t total = (size_t)N * K8;
-    for (size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-         idx += (size_t)gridDim.x * blockDim.x) {
-        const size_t n = idx / K8;
-        const int j = (int)(idx - n * K8);
-        const size_t g = n * Kg + (size_t)(j / (kGroup / 8));
-        const float s = __uint_as_float((uint32_t)scales[g] << 16);
-        const float z = SYM ? 8.0f : __uint_as_float((uint32_t)zeros[g] << 16);
-        const uint4 v = w[idx];
-        const uint32_t half[4] = {v.x, v.y, v.z, v.w};
-        uint32_t word = 0;
+//
+// Exact route, any operands: the correctly rounded division per weight.
+__device__ __forceinline__ uint32_t rtn_code_div(float b, float s, float z) {
+    const float qf = __fdiv_rn(b, s);
+    const float c = __builtin_rintf(qf) + z;
+    return (uint32_t)(qf != qf ? z : fminf(fmaxf(c, 0.0f), 15.0f));
+}
+
+// Reciprocal route, for 2^-60 <= |s| <= 2^60 and |z| <= 64 (NaN z excluded),
+// giving the same integer code as the exact route for every bf16 weight.
+// With bf16 operands the exact quotient e = w / s is either a half-integer
+// or at least 1/1020 away from every half-integer (w = mw 2^p, s = ms 2^t,
+// mw and ms in [128, 255]: e - (k + 1/2) has numerator an integer, or a
+// half-integer below 1/2, over 2 ms or 4 ms).  q = w * rcp(s) is within
+// 2 ulp of e, the fma residual w - q s is then formed with one rounding,
+// and q + residual * rcp(s) is within 2^-19 ulp of e before the fma's one
+// rounding: q' is e itself when e is a half-integer (representable), and
+// within an ulp of e, on the same side of every half-integer, otherwise;
+// for |e| < 128 an ulp is below 2^-17, so rint(q') = rint(RN(e)).  For
+// |e| >= 128 both roundings exceed 64 + 16 in magnitude with the sign of e,
+// and the code clamps to the same end.  Clamping q to +-2^30 before the
+// residual keeps an overflowed product (or an infinite weight) from turning
+// into inf - inf; a NaN weight stays NaN through the residual.  The range
+// keeps every product and residual that decides a code normal.
+__device__ __forceinline__ uint32_t rtn_code_rcp(float b, float s, float r, float z) {
+    const float q = fminf(fmaxf(b * r, -0x1p30f), 0x1p30f);
+    const float qf = __builtin_fmaf(__builtin_fmaf(-q, s, b), r, q);
+    const float c = __builtin_rintf(qf) + z;
+    return (uint32_t)(qf != qf ? z : fminf(fmaxf(c, 0.0f), 15.0f));
+}
+
+// Four consecutive packed words per thread: four 16-byte weight loads (64
+// contiguous bytes) and, when the output is 16-byte aligned, one 16-byte
+// store.  Word j of row n is word n K/8 + j of the flat output, and since
+// K/8 is a multiple of 16 the four words 4t .. 4t + 3 lie in one group,
+// group t / 4 of the flat [N][K/128] scales: one scale, zero-point and
+// reciprocal per thread.
+template <bool SYM, bool V16>
+__global__ __launch_bounds__(256) void k_quantize_pack(const uint4 *__restrict__ w,
+                                                       const uint16_t *__restrict__ scales,
+                                                       const uint16_t *__restrict__ zeros,
+                                                       uint32_t *__restrict__ packed, size_t quads) {
+    for (size_t t = (size_t)blockIdx.x * 256 + threadIdx.x; t < quads; t += (size_t)gridDim.x * 256) {
+        uint4 v[4];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const uint32_t b = (i & 1) ? (half[i >> 1] & 0xFFFF0000u) : (half[i >> 1] << 16);
-            const float qf = __fdiv_rn(__uint_as_float(b), s);
-            float c = __builtin_rintf(qf) + z;
-            c = qf != qf ? z : fminf(fmaxf(c, 0.0f), 15.0f);
-            word |= (uint32_t)c << (4 * i);
+        for (int u = 0; u < 4; ++u) v[u] = w[4 * t + u];
+        const float s = __uint_as_float((uint32_t)scales[t >> 2] << 16);
+        const float z = SYM ? 8.0f : __uint_as_float((uint32_t)zeros[t >> 2] << 16);
+        uint32_t word[4] = {0, 0, 0, 0};
+        const float as = fabsf(s);
+        if (as >= 0x1p-60f && as <= 0x1p60f && fabsf(z) <= 64.0f) {
+            const float r = __builtin_amdgcn_rcpf(s);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t half[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const uint32_t b = (i & 1) ? (half[i >> 1] & 0xFFFF0000u) : (half[i >> 1] << 16);
+                    word[u] |= rtn_code_rcp(__uint_as_float(b), s, r, z) << (4 * i);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const uint32_t half[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const uint32_t b = (i & 1) ? (half[i >> 1] & 0xFFFF0000u) : (half[i >> 1] << 16);
+                    word[u] |= rtn_code_div(__uint_as_float(b), s, z) << (4 * i);
+                }
+            }
         }
-        packed[idx] = word;
+        if (V16) {
+            *(uint4 *)(packed + 4 * t) = make_uint4(word[0], word[1], word[2], word[3]);
+        } else {
+#pragma unroll
+            for (int u = 0; u < 4; ++u) packed[4 * t + u] = word[u];
+        }
     }
 }
 
 hipError_t launch_quantize(const uint16_t *w, const uint16_t *scales, const uint16_t *zeros, uint32_t *packed,
                            int K, int N, hipStream_t st) {
-    const size_t words = (size_t)N * (K / 8);
-    const int grid = (int)std::min<size_t>((words + 255) / 256, 65536);
-    if (zeros) hipLaunchKernelGGL(k_quantize_pack<false>, dim3(grid), dim3(256), 0, st, (const uint4 *)w, scales, zeros, packed, K, N);
-    else hipLaunchKernelGGL(k_quantize_pack<true>, dim3(grid), dim3(256), 0, st, (const uint4 *)w, scales, zeros, packed, K, N);
+    const size_t quads = (size_t)N * (K / 32);
+    const int grid = (int)std::min<size_t>((quads + 255) / 256, 65536);
+    const bool v16 = ((uintptr_t)packed & 15) == 0;
+    auto kern = zeros ? (v16 ? k_quantize_pack<false, true> : k_quantize_pack<false, false>)
+                      : (v16 ? k_quantize_pack<true, true> : k_quantize_pack<true, false>);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(256), 0, st, (const uint4 *)w, scales, zeros, packed, quads);
     return hipGetLastError();
 }
 
