@@ -34,7 +34,10 @@ grid, GB/s) | swa1024 | swa2048 | attn-full | attn-short (the drafter's
 block attention: 32 query heads over 8 key/value heads of dimension 128, 16
 block queries, a T = 8192 cache with a symmetric window of 1024 or 2048
 tokens, full attention, and T = 700 inside the window; GB/s of the visible
-key/value span); ``--separate-qkv`` runs q, k and v as three launches;
+key/value span) | gemm128 | gemm512 | gemm2048 (diagnostic only: the
+vendor bf16 GEMM on weights already dequantized to bf16, at the same
+per-layer shapes and M, summed to a 36-layer pass); ``--separate-qkv`` runs
+q, k and v as three launches;
 ``--calibrate-copy`` runs a plain 256 MiB device copy for the HBM-traffic
 counter calibration.
 """
@@ -385,6 +388,46 @@ def bench_model(args, M=16, x_seed=3, drafter=False):
     print(json.dumps(out), flush=True)
 
 
+def bench_gemm_ceiling(args, M):
+    """Diagnostic only, never part of the path: the vendor bf16 GEMM
+    (torch.matmul -> hipBLASLt) on weights already dequantized to bf16, at
+    the decoder's per-layer shapes (q|k|v as one 2560 x 6144 product, o,
+    gate|up, down) and M rows.  Reports each shape's time and TFLOP/s and the
+    36-layer pass those times add up to, next to which the fused W4A16
+    kernel's prefill pass can be read.  Weights rotate over > 600 MB of
+    copies; both operands are contiguous row-major (x [M, K] @ w [K, N])."""
+    import torch
+
+    from synth import gen
+    torch.cuda.set_device(0)
+    stream = torch.cuda.Stream()
+    shapes = [("q|k|v", 2560, 6144), ("o", 4096, 2560), ("gate|up", 2560, 19456), ("down", 9728, 2560)]
+    g = torch.Generator(device="cuda").manual_seed(6)
+    out, pass_us, pass_flops = {}, 0.0, 0
+    for name, K, N in shapes:
+        copies = max(2, -(-600_000_000 // (2 * K * N)))
+        ws = [torch.randn((K, N), device="cuda", generator=g).mul_(0.02).to(torch.bfloat16) for _ in range(copies)]
+        x = torch.randn((M, K), device="cuda", generator=g).to(torch.bfloat16)
+        y = torch.empty((M, N), device="cuda", dtype=torch.bfloat16)
+        with torch.cuda.stream(stream):
+            for w in ws:
+                torch.matmul(x, w, out=y)                 # library set-up outside the capture
+        stream.synchronize()
+        calls = [(lambda w=w: torch.matmul(x, w, out=y)) for w in ws]
+        us, gr = graph_time_us(torch, stream, calls, reps=max(5, min(50, args.steps // len(calls))))
+        del gr, ws
+        torch.cuda.empty_cache()
+        tfs = 2 * M * K * N / (us * 1e-6) / 1e12
+        out[name] = {"K": K, "N": N, "us": round(us, 3), "TFLOPs": round(tfs, 1),
+                     "pct_of_peak_bf16": round(100 * tfs / PEAK_BF16_TFLOPS, 2)}
+        pass_us += us * gen.N_LAYERS
+        pass_flops += 2 * M * K * N * gen.N_LAYERS
+    tfs = pass_flops / (pass_us * 1e-6) / 1e12
+    print(json.dumps({"workload": f"bf16 GEMM on pre-dequantized weights (diagnostic ceiling), M={M}",
+                      "shapes": out, "pass_us": round(pass_us, 1), "pass_TFLOPs": round(tfs, 1),
+                      "pass_pct_of_peak_bf16": round(100 * tfs / PEAK_BF16_TFLOPS, 2)}), flush=True)
+
+
 def bench_quantize(args):
     """Fixed-grid RTN quantize + pack of the fused gate+up weight (N = 19456,
     K = 2560) from bf16: HBM-bound, reports GB/s of algorithmic bytes (bf16
@@ -591,6 +634,8 @@ def main():
     if args.workload.startswith("prefill"):
         # chunked-prefill regime: M rows through every linear of the model
         return bench_model(args, M=int(args.workload[len("prefill"):]), x_seed=4)
+    if args.workload.startswith("gemm"):
+        return bench_gemm_ceiling(args, M=int(args.workload[len("gemm"):]))
     if args.workload == "model":
         return bench_model(args)
     if args.workload == "drafter":
