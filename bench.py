@@ -175,10 +175,12 @@ def host_cores():
         return os.cpu_count() or 1
 
 
-def cpu_baseline(case, budget_s=12.0):
+def cpu_baseline(case, budget_s=12.0, y_gpu=None):
     """Time the oracle (as it stands) on the host cores on whole calls, with
     the BLAS threads set to the cores of the affinity mask; the unpack +
-    dequantize step is also timed on its own (the rest is the fp64 matmul)."""
+    dequantize step is also timed on its own (the rest is the fp64 matmul).
+    With ``y_gpu`` (bf16 bits of the timed kernel's output), every element of
+    it is checked against the last timed oracle call, by the tests' rule."""
     from oracle import qlin_ref as ref
     cores = host_cores()
     try:
@@ -190,7 +192,7 @@ def cpu_baseline(case, budget_s=12.0):
     t_start = time.perf_counter()
     while time.perf_counter() - t_start < budget_s and len(times) < 50:
         t0 = time.perf_counter()
-        ref.forward(case["x"], case["packed"], case["scales"], case["zeros"])
+        y_ref = ref.forward(case["x"], case["packed"], case["scales"], case["zeros"])
         times.append(time.perf_counter() - t0)
         if len(deq) < 3:
             t0 = time.perf_counter()
@@ -200,7 +202,13 @@ def cpu_baseline(case, budget_s=12.0):
         limiter.unregister()
     t, td = float(np.median(times)), float(np.median(deq))
     b = algorithmic_bytes(case["M"], case["K"], case["N"])
+    parity = None
+    if y_gpu is not None:
+        c = ref.compare(y_gpu, y_ref)
+        parity = {"outputs": int(y_gpu.size), "ok": c["ok"], "nbad": c["nbad"],
+                  "worst_err_over_tol": round(c["worst"], 4), "max_abs_err": c["max_abs"]}
     return {"value": round(b / t / 1e9, 4), "unit": "GB/s", "cores": int(cores), "kind": "oracle",
+            "timed_output_vs_oracle": parity,
             "sample": f"{len(times)} whole oracle calls of the M={case['M']} K={case['K']} N={case['N']} "
                       f"linear (median {t:.3f} s each: unpack + dequantize {td:.3f} s in numpy, one thread; "
                       f"fp64 matmul {max(t - td, 0.0):.3f} s on up to {cores} BLAS threads)",
@@ -591,6 +599,7 @@ def linear_rate(case, steps, warmup, path=0, split=0):
     torch.cuda.synchronize()
     ms_step = ev0.elapsed_time(ev1) / steps
     gbs = bytes_step / (ms_step * 1e-3) / 1e9
+    y_bits = y.view(torch.int16).cpu().numpy().view(np.uint16)     # the last timed step's output
 
     # eager launches from Python, for reference (host-launch bound for small kernels)
     ev2 = torch.cuda.Event(enable_timing=True)
@@ -609,7 +618,7 @@ def linear_rate(case, steps, warmup, path=0, split=0):
     del lins
     torch.cuda.empty_cache()
     return {"ms_step": ms_step, "GBps": gbs, "plan": plan, "R": R, "bytes": bytes_step, "eager_us": eager_us,
-            "stream": stream, "clocks": clocks.summary()}
+            "stream": stream, "clocks": clocks.summary(), "y_bits": y_bits}
 
 
 def main():
@@ -716,7 +725,7 @@ def main():
                      "avg_launch_us": round(ms_step * 1e3, 3)},
     }
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(case)
+        out["cpu_baseline"] = cpu_baseline(case, y_gpu=r["y_bits"])
     print(json.dumps(out), flush=True)
 
 

@@ -9,6 +9,7 @@ import sys
 import threading
 import time
 
+import numpy as np
 import pytest
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -67,3 +68,19 @@ def test_clock_sampler_without_tables_is_empty():
     with c:
         pass
     assert c.summary() == {}
+
+
+def test_cpu_baseline_checks_the_timed_output():
+    """The cpu_baseline leg compares the timed kernel's output with its own
+    oracle call: a planted one-element error is reported, a faithful output
+    passes."""
+    from oracle import qlin_ref as ref
+    from synth import gen
+    c = gen.random_case(1, 4, 256, 64)
+    y = ref.rne_bf16(ref.forward(c["x"], c["packed"], c["scales"], c["zeros"]).astype(np.float32).astype(np.float64))
+    good = bench.cpu_baseline(c, budget_s=0.1, y_gpu=y.astype(np.uint16))["timed_output_vs_oracle"]
+    assert good["ok"] and good["outputs"] == 4 * 64
+    bad = y.astype(np.uint16)
+    bad[1, 3] ^= 0x0100
+    r = bench.cpu_baseline(c, budget_s=0.1, y_gpu=bad)["timed_output_vs_oracle"]
+    assert not r["ok"] and r["nbad"] == 1
