@@ -78,15 +78,25 @@ def kernel_family(kernel):
     return "tiled" if kernel.startswith("k_tiled") else "linear"
 
 
+def code_only(text):
+    """C++ source text without its comments, trailing blanks and empty lines
+    (the sources hold no string literal with a comment marker in it)."""
+    import re
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(l.rstrip() for l in text.splitlines() if l.strip())
+
+
 def device_sources_hash(family="linear"):
-    """sha256 (16 hex digits) of the device sources of one kernel family, in
-    name order: identifies the kernels a stored counter summary was taken on."""
+    """sha256 (16 hex digits) of the code of the device sources of one kernel
+    family (comments left out), in name order: identifies the kernels a
+    stored counter summary was taken on."""
     import hashlib
     d = os.path.join(ROOT, "paper_2607_04244_amd", "csrc")
     h = hashlib.sha256()
     for name in sorted(KERNEL_SOURCES[family]):
-        with open(os.path.join(d, name), "rb") as f:
-            h.update(name.encode() + b"\0" + f.read())
+        with open(os.path.join(d, name), encoding="utf-8") as f:
+            h.update(name.encode() + b"\0" + code_only(f.read()).encode())
     return h.hexdigest()[:16]
 
 

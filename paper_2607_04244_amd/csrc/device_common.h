@@ -199,7 +199,10 @@ __device__ inline void valu_dequant(uint32_t P, const ValuDeq &d, const ExtractC
 // load before each later LDS read.  The caller waits for it explicitly
 // (s_waitcnt vmcnt) before the barrier that publishes the data; loads the
 // compiler does track and issues later are younger, so its own waits stay
-// sufficient.
+// sufficient.  These statements set m0 themselves and list it as clobbered;
+// the compiler warns that it may not preserve a reserved register across
+// them, which matters only if it kept a value of its own in m0: the
+// generated code of every kernel here has no other m0 access.
 __device__ inline void load_lds_x16(const void *src, const uint4 *lds_dst) {
     const uint32_t m0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)lds_dst);
     asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" :: "s"(m0), "v"(src) : "memory", "m0");

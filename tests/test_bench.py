@@ -84,3 +84,9 @@ def test_cpu_baseline_checks_the_timed_output():
     bad[1, 3] ^= 0x0100
     r = bench.cpu_baseline(c, budget_s=0.1, y_gpu=bad)["timed_output_vs_oracle"]
     assert not r["ok"] and r["nbad"] == 1
+
+
+def test_source_hash_ignores_comments_only():
+    src = "int a; // note\n/* block\n comment */ int b;\n\n"
+    assert bench.code_only(src) == bench.code_only("int a;\n int b;")
+    assert bench.code_only(src) != bench.code_only("int a; int c;")
