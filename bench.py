@@ -531,12 +531,18 @@ def bench_attention(args, name):
         t_start = time.perf_counter()
         while time.perf_counter() - t_start < 10.0 and len(times) < 20:
             t0 = time.perf_counter()
-            ar.swa_attention(c["q"], c["k"], c["v"], W)
+            o_ref = ar.swa_attention(c["q"], c["k"], c["v"], W)
             times.append(time.perf_counter() - t0)
         t = float(np.median(times))
         threads = host_cores()
+        # the last timed call's output against the oracle (every copy of the cache holds the same data)
+        o_gpu = ar.bf16_to_f64(out.view(torch.int16).cpu().numpy().view(np.uint16))
+        vmax = float(np.abs(ar.bf16_to_f64(c["v"])).max())
+        err = float(np.abs(o_gpu - o_ref).max())
         res["cpu_baseline"] = {"value": round(nbytes / t / 1e9, 4), "unit": "GB/s", "cores": int(threads),
                                "kind": "oracle",
+                               "timed_output_vs_oracle": {"outputs": int(o_gpu.size), "max_abs_err": err,
+                                                          "max_abs_err_over_max_abs_v": round(err / vmax, 6)},
                                "sample": f"{len(times)} whole oracle calls (median {t:.3f} s; float64 numpy, "
                                          f"matmuls on up to {threads} BLAS threads)"}
     print(json.dumps(res), flush=True)
