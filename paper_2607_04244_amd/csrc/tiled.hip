@@ -204,10 +204,7 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     // LDS slot of this lane's operand read: row 16 ms + lm, chunk 4 j + lg
     auto xslot = [&](int ms, int j) { return ms * 256 + lm * 16 + ((4 * j + lg) ^ lm); };
 
-    auto compute = [&](int buf) {
-        uint4 cw[NW];
-        uint32_t sw[NW];
-        read_w(buf, cw, sw);
+    auto compute = [&](int buf, const uint4 (&cw)[NW], const uint32_t (&sw)[NW]) {
         MfmaDeq d[NW];
 #pragma unroll
         for (int t = 0; t < NW; ++t) d[t] = mfma_setup(sw[t], dsel);
@@ -235,7 +232,10 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     // one barrier both publishes group kb and shows that every wave is done
     // with the previous step's buffer, which the step refills with group
     // kb + S - 1 (past the last group the loads reload it into a buffer
-    // nobody reads) before computing group kb.
+    // nobody reads) before computing group kb.  A wave's weight blocks and
+    // s|z words are its own loads, in LDS once its own wait is over: it reads
+    // them before the barrier, which only the x tile (loaded by all the
+    // waves) needs, so that LDS round trip overlaps the wait for the others.
     constexpr int kIssued = kXLoads + 2 * NW;
     constexpr int S = kTiledStages;
     static_assert(S >= 2, "the pipeline needs two stages");
@@ -247,11 +247,14 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     int buf = 0;
     for (int kb = g0; kb <= g1; ++kb) {
         asm volatile("s_waitcnt vmcnt(%0)" :: "n"((S - 2) * kIssued) : "memory");
+        uint4 cw[NW];
+        uint32_t sw[NW];
+        read_w(buf, cw, sw);
         lds_barrier();                        // group kb is in LDS for every wave; buffer nb is free
         const int nb = buf == 0 ? S - 1 : buf - 1;             // (kb - g0 + S - 1) % S
         load_x(min(kb + S - 1, g1), nb);
         load_w(min(kb + S - 1, g1), nb);
-        compute(buf);
+        compute(buf, cw, sw);
         buf = buf == S - 1 ? 0 : buf + 1;
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // the reloads past the end
