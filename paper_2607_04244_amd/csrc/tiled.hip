@@ -236,6 +236,9 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
     // s|z words are its own loads, in LDS once its own wait is over: it reads
     // them before the barrier, which only the x tile (loaded by all the
     // waves) needs, so that LDS round trip overlaps the wait for the others.
+    // For the two taller block shapes the wave also sends its next weight
+    // loads before the barrier (measured faster for them, slower for 64 x
+    // 128 blocks).
     constexpr int kIssued = kXLoads + 2 * NW;
     constexpr int S = kTiledStages;
     static_assert(S >= 2, "the pipeline needs two stages");
@@ -250,10 +253,18 @@ __global__ void __launch_bounds__(kTiledWaves * WS * 64, MSW * NT <= 8 ? 2 : 1) 
         uint4 cw[NW];
         uint32_t sw[NW];
         read_w(buf, cw, sw);
-        lds_barrier();                        // group kb is in LDS for every wave; buffer nb is free
         const int nb = buf == 0 ? S - 1 : buf - 1;             // (kb - g0 + S - 1) % S
-        load_x(min(kb + S - 1, g1), nb);
-        load_w(min(kb + S - 1, g1), nb);
+        if constexpr (MSW >= 6) {
+            // the wave's own blocks in nb were read (and waited for) in the
+            // previous step: their refill can go out before the barrier
+            load_w(min(kb + S - 1, g1), nb);
+            lds_barrier();                    // group kb is in LDS for every wave; buffer nb is free
+            load_x(min(kb + S - 1, g1), nb);
+        } else {
+            lds_barrier();
+            load_x(min(kb + S - 1, g1), nb);
+            load_w(min(kb + S - 1, g1), nb);
+        }
         compute(buf, cw, sw);
         buf = buf == S - 1 ? 0 : buf + 1;
     }
