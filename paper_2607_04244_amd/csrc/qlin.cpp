@@ -205,12 +205,13 @@ namespace {
 
 // The workspace capacity a plan may assume when nothing limits it: partial
 // sums for any split the decode planner considers (S * M up to the handle's
-// cap_rows), and one 64 x 128 fp32 block per compute unit for a K-split
-// tiled launch.
+// cap_rows), and four 64 x 128 fp32 blocks per compute unit for a K-split
+// tiled launch (32 MiB with 256 CUs: the measured splits of the deep layers
+// at M = 512 .. 1024 need up to 31.5 MB).
 void full_capacity(Target &t) {
     const int rows = t.mem[0]->cap_rows;
     const size_t dec = std::min(2 * (size_t)rows * (size_t)t.N, kMaxWsBytes / 4);
-    t.cap_floats = std::max(dec, std::min((size_t)t.num_cu * 64 * 128, kMaxWsBytes / 4));
+    t.cap_floats = std::max(dec, std::min((size_t)t.num_cu * 4 * 64 * 128, kMaxWsBytes / 4));
     t.cap_counters = std::min(std::max(t.Nt, t.num_cu), kMaxCounters);
 }
 
@@ -356,6 +357,21 @@ int64_t tiled_col_blocks(const Target &t, int nt) {
     return g;
 }
 
+// Tiled plans measured on MI355X (256 compute units) for the 4B decoder's
+// deep and narrow layers where the model below picks a slower one: every
+// block shape with every K split from 1 to 6 was timed (HIP-graph replays
+// over > 0.8 GB of rotating weight copies) at M = 512 and 1024.  Down
+// (9728 -> 2560): 53.9 -> 42.4 us at M = 512, 85.3 -> 62.8 us at M = 1024;
+// o (4096 -> 2560): 25.1 -> 23.8 us and 39.1 -> 35.1 us.  Each entry is used
+// only where the workspace holds its partial blocks.
+struct TunedTiled { int m_lo, m_hi, K, N, shape, S; };
+constexpr TunedTiled kTunedTiled[] = {
+    {385, 640, 9728, 2560, 1, 3},     // down: 64 x 128 blocks, 3 K chunks
+    {385, 640, 4096, 2560, 1, 3},     // o
+    {769, 1280, 9728, 2560, 0, 3},    // down: 128 x 256 blocks, 3 K chunks
+    {769, 1280, 4096, 2560, 2, 2},    // o: 96 x 256 blocks, 2 K chunks
+};
+
 // TILED plan: one launch over all M rows and all members.  The block shape
 // minimises (blocks per compute unit, rounded up) x (time of one block), with
 // the block times measured on MI355X relative to the 128 x 256 shape (same
@@ -394,13 +410,26 @@ int make_tiled_plan(const Target &t, int64_t split_k, int64_t M, Plan *p) {
         const double c = (double)((blocks_of(i) + t.num_cu - 1) / t.num_cu) * kBlockTime[i];
         if (c < best) { best = c; best_i = i; }
     }
-    // A K split, when that leaves more than half the CUs idle (or when one is
-    // asked for) and the workspace holds its partial blocks.  Time model in
-    // us: a pipeline ramp plus a time per 128-wide group of K per block with
-    // every CU busy (128 x 256: 2.28, 64 x 128: 0.97, 96 x 256: 2.17), times
-    // the rounds of work items over the CUs; a split adds the exchange: ~3 us
-    // of latency plus the partial blocks written and read back at ~4 TB/s.
-    if (split_k > 1 || (split_k == 0 && blocks_of(best_i) * 2 <= t.num_cu)) {
+    const TunedTiled *tuned = nullptr;
+    if (split_k == 0 && forced < 0 && t.num_cu == 256)
+        for (const TunedTiled &e : kTunedTiled)
+            if (M >= e.m_lo && M <= e.m_hi && t.K == e.K && t.N == e.N) {
+                const TiledShape c = kTiledShapes[e.shape];
+                const int64_t blocks = blocks_of(e.shape);
+                if (blocks <= t.cap_counters && (double)e.S * blocks * 16 * c.msw * 64 * c.nt <= (double)t.cap_floats)
+                    tuned = &e;
+            }
+    // A measured plan if one fits; else a K split, when that leaves more than
+    // half the CUs idle (or when one is asked for) and the workspace holds
+    // its partial blocks.  Time model in us: a pipeline ramp plus a time per
+    // 128-wide group of K per block with every CU busy (128 x 256: 2.28,
+    // 64 x 128: 0.97, 96 x 256: 2.17), times the rounds of work items over the
+    // CUs; a split adds the exchange: ~3 us of latency plus the partial
+    // blocks written and read back at ~4 TB/s.
+    if (tuned) {
+        best_i = tuned->shape;
+        best_s = tuned->S;
+    } else if (split_k > 1 || (split_k == 0 && blocks_of(best_i) * 2 <= t.num_cu)) {
         constexpr double kRamp = 2.0, kGroupTime[] = {2.28, 0.97, 2.17}, kExchange = 3.0, kPartialBw = 4.0e6;
         static_assert(sizeof kGroupTime / sizeof kGroupTime[0] == kShapes, "");
         best_i = -1;

@@ -92,3 +92,25 @@ def test_decoder_shape_at_prefill_rows(name, M):
     plan = lin.plan(M)
     lin.close()
     check(y, w, x, M, M, f"{name} M={M} ({plan})")
+
+
+@pytest.mark.parametrize("M,name,expect", [
+    (512, "down", "kernel=k_tiled<4,2> grid=480 block=256 split=3"),
+    (512, "o", "kernel=k_tiled<4,2> grid=480 block=256 split=3"),
+    (1024, "down", "kernel=k_tiled<8,4> grid=240 block=512 split=3"),
+    (1024, "o", "kernel=k_tiled<6,4> grid=224 block=512 split=2"),
+])
+def test_measured_tiled_split_with_caller_workspace(M, name, expect):
+    """The deep and narrow layers at M = 512 and 1024 take the measured K
+    split when the caller's workspace holds it (a handle's own workspace is
+    sized for decode and keeps the unsplit plan): the plan is the table's,
+    and every sampled output matches the oracle."""
+    w = weights(21, name)
+    lin = qlin.QLinear(w["packed"], w["scales"], w["zeros"])
+    need, plan = qlin.group_plan([lin], M)
+    assert expect in plan and need > 0, plan
+    x = gen.model_activations(4, M, w["K"])
+    y = host_bits(qlin.forward_group([lin], dev(x), workspace=qlin.new_workspace(need))[0])
+    torch.cuda.synchronize()
+    lin.close()
+    check(y, w, x, M, M + 7, f"{name} M={M} ({plan})")
