@@ -360,9 +360,12 @@ int64_t tiled_col_blocks(const Target &t, int nt) {
 // Tiled plans measured on MI355X (256 compute units) for the 4B decoder's
 // deep and narrow layers where the model below picks a slower one: every
 // block shape with every K split from 1 to 6 was timed (HIP-graph replays
-// over > 0.8 GB of rotating weight copies) at M = 512 and 1024.  Down
-// (9728 -> 2560): 53.9 -> 42.4 us at M = 512, 85.3 -> 62.8 us at M = 1024;
-// o (4096 -> 2560): 25.1 -> 23.8 us and 39.1 -> 35.1 us.  Each entry is used
+// over > 0.8 GB of rotating weight copies) at M = 128, 512, 1024 and 2048.
+// Down (9728 -> 2560): 53.9 -> 42.4 us at M = 512, 85.3 -> 62.8 us at
+// M = 1024; o (4096 -> 2560): 25.1 -> 23.8 us and 39.1 -> 35.1 us.  At
+// M = 2048 the model's choices were the fastest; at M = 128 the one
+// candidate that won alone (gate|up as 128 x 256 blocks in 3 K chunks,
+// 28.1 against 29.1 us) made the whole pass 2% slower.  Each entry is used
 // only where the workspace holds its partial blocks.
 struct TunedTiled { int m_lo, m_hi, K, N, shape, S; };
 constexpr TunedTiled kTunedTiled[] = {
