@@ -114,3 +114,18 @@ def test_measured_tiled_split_with_caller_workspace(M, name, expect):
     torch.cuda.synchronize()
     lin.close()
     check(y, w, x, M, M + 7, f"{name} M={M} ({plan})")
+
+
+@pytest.mark.parametrize("M,name", [(397, "down"), (639, "o"), (771, "down"), (1279, "o")])
+def test_measured_tiled_split_at_ragged_rows(M, name):
+    """The measured plans at the edges of their row ranges, where the last
+    row block is partial: every sampled output against the oracle."""
+    w = weights(22, name)
+    lin = qlin.QLinear(w["packed"], w["scales"], w["zeros"])
+    need, plan = qlin.group_plan([lin], M)
+    assert "split=1 " not in plan and need > 0, plan
+    x = gen.model_activations(4, M, w["K"])
+    y = host_bits(qlin.forward_group([lin], dev(x), workspace=qlin.new_workspace(need))[0])
+    torch.cuda.synchronize()
+    lin.close()
+    check(y, w, x, M, M + 11, f"{name} M={M} ({plan})")
